@@ -1,0 +1,381 @@
+#!/usr/bin/env python3
+"""Benchmark of the ODA decode-step hot path on one MI355X.
+
+A step is one pass of the whole path over one batch: Local decode attention
+for every layer and request, the recall gate (score + device predicate +
+compaction), and Full decode attention for the flagged requests only, all on
+one stream.  The recall rate rho is swept by the threshold tau (calibrated on
+the gate's scores over the K timed steps), and compared against the
+always-Full baseline (Full for every request, no Local, no gate).
+
+Timing: every step is bracketed by HIP events on the stream the library
+launches on.  Headline ("cold") numbers read a 1 GiB scratch buffer between
+steps, outside the events, so the 256 MB Infinity Cache holds no KV or gate
+weights at the start of a step; "warm" numbers run the K steps back to back.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config llama3-8b] [--head paper|mlp]
+
+Prints one JSON line (see the design doc for the fields).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode-attn µs/step + achieved HBM GB/s vs always-Full, recall rate 0-100%"
+HBM_PEAK_GBS = 8000.0
+HEADLINE_RHO = 0.1
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class StackState:
+    """Device buffers of one layer group (shared block table)."""
+
+    def __init__(self, P, wl, stack, seq, table, num_blocks, mb, seed, dev, split_blocks):
+        import torch
+
+        import oda_synth as S
+        self.stack = stack
+        L, B, Hq, Hkv, D = stack.num_layers, wl.batch, wl.num_q_heads, wl.num_kv_heads, wl.head_dim
+        self.shape = P.Shape(L, B, Hq, Hkv, D, mb, int(max(seq)), num_blocks, split_blocks)
+        self.k = torch.empty((L, num_blocks, Hkv, D // 8, 16, 8), dtype=torch.bfloat16, device=dev)
+        self.v = torch.empty((L, num_blocks, Hkv, D, 16), dtype=torch.bfloat16, device=dev)
+        S.fill_normal_bf16_(self.k, seed, S.STREAM_K + 100 * len(stack.name))
+        S.fill_normal_bf16_(self.v, seed, S.STREAM_V + 100 * len(stack.name))
+        q = S.normal_bf16(S.rng(seed + len(stack.name), S.STREAM_Q), (L, B, Hq, D))
+        self.q = torch.from_numpy(q.view(np.int16)).to(dev)
+        self.table = table
+        self.seq = seq
+        self.inp = P.inputs(self.q, self.k, self.v, table, seq, 1.0 / math.sqrt(D))
+        self.out = torch.zeros((L, B, Hq, D), dtype=torch.float32, device=dev)
+        self.lse = torch.zeros((L, B, Hq), dtype=torch.float32, device=dev)
+        loc_w = stack.native_window if not stack.gated else stack.local_window
+        loc_s = 0 if not stack.gated else stack.local_sink
+        self.local_args = (loc_s, loc_w)
+        self.ws_local = torch.empty(P.attn_workspace_size(self.shape, loc_s, loc_w), dtype=torch.uint8, device=dev)
+        self.ws_full = torch.empty(P.attn_workspace_size(self.shape, 0, stack.native_window), dtype=torch.uint8,
+                                   device=dev)
+
+
+class Bench:
+    def __init__(self, wl, head, seed, steps, split_blocks=0):
+        import torch
+
+        import oda_synth as S
+        import paper_2609_20734_amd as P
+        self.P, self.torch, self.wl, self.head, self.seed, self.K = P, torch, wl, head, seed, steps
+        dev = torch.device("cuda:0")
+        self.dev = dev
+        B = wl.batch
+        if wl.seq_lens:
+            seq = np.array(wl.seq_lens, dtype=np.int32)
+        else:
+            seq = S.uniform_seq_lens(seed, B, *wl.seq_range)
+        self.seq_host = seq
+        mb = int(math.ceil(seq.max() / 16))
+        table, nb = S.paged_block_table(S.rng(seed, S.STREAM_TABLE), seq, mb, permute=wl.permute)
+        need = sum(st.num_layers for st in wl.stacks) * nb * wl.num_kv_heads * wl.head_dim * 16 * 2 * 2
+        free, total = torch.cuda.mem_get_info()
+        log(f"[bench] {wl.name}: KV {need / 1e9:.2f} GB, device free {free / 1e9:.1f} GB")
+        if need > free - 8e9:
+            raise SystemExit(f"workload needs {need / 1e9:.1f} GB of KV, only {free / 1e9:.1f} GB free")
+        self.dtable = torch.from_numpy(table).to(dev)
+        self.dseq = torch.from_numpy(seq).to(dev)
+        self.stacks = [StackState(P, wl, st, self.dseq, self.dtable, nb, mb, seed, dev, split_blocks)
+                       for st in wl.stacks]
+        # gate
+        kind = P.HEAD_PAPER if head == "paper" else P.HEAD_MLP
+        params = S.gate_params(seed, head, wl.d_model, wl.d_hidden)
+        self.params = torch.from_numpy(params).to(dev)
+        self.gate = P.gate_desc(kind, wl.d_model, wl.d_hidden, self.params, 1e-6)
+        h, e, l = S.gate_inputs(seed, steps, B, wl.d_model)
+        self.h = torch.from_numpy(h).to(dev)
+        self.e = torch.from_numpy(e).to(dev)
+        self.l = torch.from_numpy(l).to(dev)
+        self.ws_gate = torch.empty(P.gate_workspace_size(self.gate, B), dtype=torch.uint8, device=dev)
+        self.score = torch.zeros(B, dtype=torch.float32, device=dev)
+        self.flags = torch.zeros(B, dtype=torch.int32, device=dev)
+        self.work = torch.zeros(B, dtype=torch.int32, device=dev)
+        self.n_work = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.counter = torch.zeros(1, dtype=torch.int64, device=dev)
+        # 1 GiB read between steps evicts the 256 MB Infinity Cache with clean lines
+        # (a write flush would leave dirty lines for the next step to write back)
+        self.flush_buf = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+
+    def flush(self):
+        self.flush_buf.max()
+
+    # -- calls ---------------------------------------------------------------
+    def step_calls(self, tau, forced=None):
+        """Per step t: the list of pre-marshalled calls of one decode step."""
+        P = self.P
+        local = [P.prepare_local(s.shape, s.inp, *s.local_args, s.out, s.lse, s.ws_local) for s in self.stacks]
+        full = [P.prepare_full(s.shape, s.inp, s.stack.native_window, None, self.work, self.n_work, s.out, s.lse,
+                               s.ws_full) for s in self.stacks]
+        steps = []
+        for t in range(self.K):
+            fo = None if forced is None else forced[t]
+            g = P.prepare_gate(self.gate, self.wl.batch, self.h[t], self.e[t], self.l[t], tau, fo, self.score,
+                               self.flags, self.work, self.n_work, self.counter, self.ws_gate)
+            steps.append(local + [g] + full)
+        return steps
+
+    def full_calls(self):
+        P = self.P
+        full = [P.prepare_full(s.shape, s.inp, s.stack.native_window, None, None, None, s.out, s.lse, s.ws_full)
+                for s in self.stacks]
+        return [full] * self.K
+
+    def scores(self):
+        """Gate scores of all K steps (tau = +inf), for threshold calibration."""
+        out = np.zeros((self.K, self.wl.batch))
+        for t in range(self.K):
+            self.P.recall_gate(self.gate, self.wl.batch, self.h[t], self.e[t], self.l[t], math.inf, None,
+                               self.score, self.flags, None, None, None, self.ws_gate)
+            out[t] = self.score.cpu().numpy()
+        return out
+
+    # -- timing --------------------------------------------------------------
+    def timed(self, steps, warmup, cold=True):
+        torch = self.torch
+        for t in range(warmup):
+            for c in steps[t % len(steps)]:
+                c()
+        torch.cuda.synchronize()
+        self.counter.zero_()
+        K = len(steps)
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+        wall0 = time.perf_counter()
+        t_all0 = torch.cuda.Event(enable_timing=True)
+        t_all1 = torch.cuda.Event(enable_timing=True)
+        t_all0.record()
+        for t in range(K):
+            if cold:
+                self.flush()
+            evs[t][0].record()
+            for c in steps[t]:
+                c()
+            evs[t][1].record()
+        t_all1.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+        per = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])      # us
+        return dict(us_mean=float(per.mean()), us_median=float(np.median(per)), us_min=float(per.min()),
+                    us_max=float(per.max()), bracket_us=float(t_all0.elapsed_time(t_all1) * 1e3 / K),
+                    wall_us=wall * 1e6 / K, per_step=per, recalled=int(self.counter.item()))
+
+    def kernel_time(self, calls, reps, cold=True):
+        """Mean duration (us) of one call bracketed by events on its stream."""
+        torch = self.torch
+        for c in calls:
+            c()
+        torch.cuda.synchronize()
+        durs = []
+        for _ in range(reps):
+            if cold:
+                self.flush()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for c in calls:
+                c()
+            b.record()
+            torch.cuda.synchronize()
+            durs.append(a.elapsed_time(b) * 1e3)
+        return float(np.mean(durs))
+
+
+def taus_for(scores, rhos):
+    flat = np.sort(scores.reshape(-1))[::-1]
+    N = len(flat)
+    out = {}
+    for rho in rhos:
+        m = int(round(rho * N))
+        if m <= 0:
+            out[rho] = math.inf
+        elif m >= N:
+            out[rho] = -math.inf
+        else:
+            out[rho] = float(0.5 * (flat[m - 1] + flat[m]))
+    return out
+
+
+def bytes_for(wl, seq, flagged_frac_per_step, head):
+    """Average algorithmic bytes per step given the realised per-step flag sets."""
+    from paper_2609_20734_amd import ledger as LG
+    B = wl.batch
+    local = sum(LG.attention_bytes(seq, *(st.local_sink, st.local_window) if st.gated else (0, st.native_window),
+                                   st.num_layers, wl.num_q_heads, wl.num_kv_heads, wl.head_dim)["total"]
+                for st in wl.stacks)
+    gate = LG.gate_bytes(head, B, wl.d_model, wl.d_hidden)["total"]
+    full_all = [sum(LG.attention_bytes(seq, 0, st.native_window, st.num_layers, wl.num_q_heads, wl.num_kv_heads,
+                                       wl.head_dim, requests=[b])["total"] for st in wl.stacks) for b in range(B)]
+    return local, gate, full_all
+
+
+def cpu_baseline(b, rho, budget_s=15.0):
+    """The fp64 oracle timed on a bounded sample of the same step, 1 thread."""
+    from threadpoolctl import threadpool_limits
+
+    from oracle import attention as OA
+    from oracle import gate as OG
+    wl = b.wl
+    st = b.stacks[-1]
+    L = st.stack.num_layers
+    seq = b.seq_host
+    with threadpool_limits(limits=1):
+        # gate (one step)
+        t0 = time.perf_counter()
+        params = b.params.cpu().numpy()
+        h, e, l = (x[0].cpu().numpy().astype(np.float64) for x in (b.h, b.e, b.l))
+        if b.head == "paper":
+            OG.paper_head_score(params, wl.d_model, wl.d_hidden, 1e-6, h, e, l)
+        else:
+            OG.mlp_score(params, wl.d_model, wl.d_hidden, l)
+        t_gate = time.perf_counter() - t0
+        # per layer: copy the layer's cache once, then Local and Full for every request
+        q_all = b.stacks[-1].q.cpu().numpy().view(np.uint16)
+        table = b.dtable.cpu().numpy()
+        t_local = t_full = 0.0
+        layers = 0
+        for layer in range(L):
+            kl = st.k[layer:layer + 1].cpu().view(b.torch.int16).numpy().view(np.uint16)
+            vl = st.v[layer:layer + 1].cpu().view(b.torch.int16).numpy().view(np.uint16)
+            ql = q_all[layer:layer + 1]
+            s_, w_ = st.local_args
+            t0 = time.perf_counter()
+            OA.decode_attention(ql, kl, vl, table, seq, lambda n: OA.local_set(n, s_, w_), 1 / math.sqrt(wl.head_dim))
+            t1 = time.perf_counter()
+            OA.decode_attention(ql, kl, vl, table, seq, lambda n: OA.native_window_set(n, st.stack.native_window),
+                                1 / math.sqrt(wl.head_dim))
+            t2 = time.perf_counter()
+            t_local += t1 - t0
+            t_full += t2 - t1
+            layers += 1
+            if t_local + t_full + t_gate > budget_s:
+                break
+    scale = wl.num_layers / layers
+    per_step = t_gate + scale * (t_local + rho * t_full)
+    return dict(value=per_step * 1e6, unit="us/step", cores=1, kind="oracle",
+                sample=f"{layers} of {wl.num_layers} layers (Local + Full, all {wl.batch} requests) and one gate "
+                       f"evaluation, fp64 NumPy, 1 thread; extrapolated linearly to {wl.num_layers} layers at "
+                       f"rho={rho} (Full time weighted by rho)",
+                measured_s=t_gate + t_local + t_full)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="llama3-8b")
+    ap.add_argument("--head", default="paper", choices=["paper", "mlp"])
+    ap.add_argument("--seed", type=int, default=1234)
+    ap.add_argument("--split-blocks", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--warm", action="store_true", help="also time back-to-back (warm) steps")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}), flush=True)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_20734_amd import workloads as WL
+    wl = WL.ALL[args.config]
+    K = args.steps
+    b = Bench(wl, args.head, args.seed, K, args.split_blocks)
+    P = b.P
+
+    # always-Full baseline
+    full = b.timed(b.full_calls(), args.warmup, cold=True)
+    local_b, gate_b, full_b = bytes_for(wl, b.seq_host, None, args.head)
+    bytes_full = sum(full_b)
+    log(f"[bench] always-Full {full['us_mean']:.1f} us/step ({bytes_full / full['us_mean'] / 1e3:.0f} GB/s)")
+
+    # rho sweep
+    sweep = []
+    if wl.rhos:
+        sc = b.scores()
+        taus = taus_for(sc, wl.rhos)
+        for rho in wl.rhos:
+            r = b.timed(b.step_calls(taus[rho]), args.warmup, cold=True)
+            real = r["recalled"] / (K * wl.batch)
+            step_bytes = local_b + gate_b + real * bytes_full
+            ent = dict(rho=rho, tau=taus[rho], realised_rho=real, us=r["us_mean"], us_median=r["us_median"],
+                       us_min=r["us_min"], us_max=r["us_max"], GBps=step_bytes / r["us_mean"] / 1e3,
+                       ratio=r["us_mean"] / full["us_mean"], ideal_ratio=step_bytes / bytes_full)
+            ent["linearity"] = ent["ratio"] / ent["ideal_ratio"]
+            if args.warm:
+                w = b.timed(b.step_calls(taus[rho]), args.warmup, cold=False)
+                ent["warm_us"] = w["us_mean"]
+                ent["warm_bracket_us"] = w["bracket_us"]
+            sweep.append(ent)
+            log(f"[bench] rho={rho:.3f} (real {real:.3f}) {r['us_mean']:.1f} us/step ratio {ent['ratio']:.3f} "
+                f"ideal {ent['ideal_ratio']:.3f} x{ent['linearity']:.2f} {ent['GBps']:.0f} GB/s")
+    else:
+        import oda_synth as S
+        for p in wl.bernoulli:
+            forced_np = S.bernoulli_flags(args.seed, K, wl.batch, p)
+            forced = torch.from_numpy(forced_np).to(b.dev)
+            r = b.timed(b.step_calls(0.0, forced=forced), args.warmup, cold=True)
+            real = r["recalled"] / (K * wl.batch)
+            exp_full = float(np.mean([(forced_np[t] * np.array(full_b)).sum() for t in range(K)]))
+            step_bytes = local_b + gate_b + exp_full
+            ent = dict(rho=p, realised_rho=real, us=r["us_mean"], us_median=r["us_median"], us_min=r["us_min"],
+                       us_max=r["us_max"], GBps=step_bytes / r["us_mean"] / 1e3, ratio=r["us_mean"] / full["us_mean"],
+                       ideal_ratio=step_bytes / bytes_full)
+            ent["linearity"] = ent["ratio"] / ent["ideal_ratio"]
+            sweep.append(ent)
+            log(f"[bench] p={p:.2f} (real {real:.3f}) {r['us_mean']:.1f} us/step ratio {ent['ratio']:.3f} "
+                f"ideal {ent['ideal_ratio']:.3f} x{ent['linearity']:.2f}")
+
+    # roofline of the dominant kernel: the Full split-K pass over all requests
+    fcalls = b.full_calls()[0]
+    t_full_call = b.kernel_time(fcalls, reps=max(5, min(50, K // 4)), cold=True)
+    roof = dict(bound="hbm", achieved=bytes_full / t_full_call / 1e3, peak=HBM_PEAK_GBS, unit="GB/s",
+                traffic=None)
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["kernel"] = "oda_full_decode_attn (attn_split_kernel<128> + attn_merge_kernel<128>), all requests"
+    roof["bytes_per_launch"] = bytes_full
+    roof["us_per_launch"] = t_full_call
+
+    head_ent = min(sweep, key=lambda e: abs(e["rho"] - HEADLINE_RHO)) if sweep else None
+    value = head_ent["us"] if head_ent else full["us_mean"]
+    res = {
+        "metric": METRIC, "value": round(value, 3), "unit": "us/step", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(value / 1e3, 6), "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {wl.num_layers} layers, B={wl.batch}, {wl.num_q_heads}q/{wl.num_kv_heads}kv "
+                               f"heads, D={wl.head_dim}, n={'/'.join(str(x) for x in sorted(set(b.seq_host.tolist()))[:4])}"
+                               f"{'...' if len(set(b.seq_host.tolist())) > 4 else ''}, "
+                               f"W={wl.stacks[-1].local_window}, s={wl.stacks[-1].local_sink}, paged bf16 KV "
+                               f"(block 16, permuted), {args.head} recall head {wl.d_model}->{wl.d_hidden}->1, "
+                               f"rho={head_ent['rho'] if head_ent else 1.0}, cold (Infinity Cache flushed between steps)",
+                   "head": args.head, "seed": args.seed, "split_blocks": args.split_blocks},
+        "GBps": round(head_ent["GBps"], 1) if head_ent else None,
+        "always_full_us": round(full["us_mean"], 3),
+        "always_full_GBps": round(bytes_full / full["us_mean"] / 1e3, 1),
+        "sweep": [{k: (round(v, 4) if isinstance(v, float) else v) for k, v in e.items()} for e in sweep],
+        "roofline": {k: (round(v, 4) if isinstance(v, float) else v) for k, v in roof.items()},
+    }
+    if not args.no_cpu_baseline:
+        cb = cpu_baseline(b, head_ent["rho"] if head_ent else 1.0)
+        res["cpu_baseline"] = {k: (round(v, 3) if isinstance(v, float) else v) for k, v in cb.items()}
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

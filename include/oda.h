@@ -1,0 +1,206 @@
+/*
+ * oda.h -- C ABI of the On-Demand Attention (ODA) decode-step hot path on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * One decode step of ODA (Alg. 1) runs, in stream order:
+ *   1. oda_local_decode_attn  -- attention over the Local access set S^L
+ *                                (s initial positions + a recent window of w
+ *                                positions that includes the current token;
+ *                                §2.1, access-set equation);
+ *   2. oda_recall_gate        -- the recall score q_t = R(h_{t-1}, E(x_t), h_t^L)
+ *                                (§2.1, recall-head equation; head of App. A.2,
+ *                                or a two-layer MLP stand-in) and the device
+ *                                predicate "Full iff q_t > theta or q_t is
+ *                                nonfinite" (§2.1, Alg. 1, App. A.5), written
+ *                                as per-request flags plus a compacted list;
+ *   3. oda_full_decode_attn   -- attention over the native access set, from the
+ *                                same pre-step history, for flagged requests
+ *                                only; it overwrites their rows of the output,
+ *                                so the output buffer ends up holding the
+ *                                selected branch (App. A.5, commit equation).
+ *
+ * Conventions (all entry points):
+ *   - Pointers are DEVICE pointers unless marked (host).  The caller owns every
+ *     buffer; the library never allocates, never synchronises and never copies
+ *     device memory to the host.
+ *   - Host-visible arguments are validated synchronously; on any error the call
+ *     returns a negative status and enqueues nothing.  oda_last_error() then
+ *     holds a thread-local description.
+ *   - All work is enqueued on `stream` (NULL = the default stream).
+ *   - Device-data contract (not checked): seq_lens[b] in [1, max_seq_len];
+ *     every block-table entry a request uses is in [0, num_blocks).
+ *   - The library keeps no state between calls.  Workspaces may be reused by
+ *     later calls on the same stream; calls that share a workspace must not
+ *     overlap in time.
+ *   - Results are deterministic: a fixed split order, no floating-point
+ *     atomics; reruns are bit-identical.
+ *
+ * Data layouts (bf16 = IEEE bfloat16 stored as uint16_t):
+ *   q        bf16 [L][B][Hq][D]   post-RoPE queries of the current token
+ *   k_cache  bf16 [L][num_blocks][Hkv][D/8][16][8]
+ *            paged keys, 16 positions per block; within a block and KV head,
+ *            16-byte groups of 8 consecutive dims, position-minor:
+ *            K(pos, d) = k_cache[l][blk][g][d/8][pos%16][d%8]
+ *   v_cache  bf16 [L][num_blocks][Hkv][D][16]
+ *            paged values, dims-major:  V(pos, d) = v_cache[l][blk][g][d][pos%16]
+ *            where blk = block_table[b][pos/16]
+ *   k_cur, v_cur  bf16 [L][B][Hkv][D]  (optional) the current token's candidate
+ *            K/V, not yet committed to the cache (App. A.5)
+ *   out      fp32 [L][B][Hq][D];  lse fp32 [L][B][Hq]  (natural log)
+ *   GQA: query head h reads KV head h / (Hq/Hkv)  (contiguous groups).
+ */
+#ifndef ODA_H_
+#define ODA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ODA_OK = 0,
+  ODA_ERR_NULL = -1,        /* a required pointer is NULL                      */
+  ODA_ERR_SHAPE = -2,       /* inconsistent or out-of-range sizes              */
+  ODA_ERR_UNSUPPORTED = -3, /* valid but not implemented (e.g. D not 64/128)   */
+  ODA_ERR_WORKSPACE = -4,   /* workspace NULL or smaller than required         */
+  ODA_ERR_HIP = -5          /* a kernel launch failed (hipGetLastError)        */
+} oda_status;
+
+/* Shape of one attention call (host struct).  Every layer of the stack
+ * shares B, heads, D, the block table and seq_lens. */
+typedef struct {
+  int32_t num_layers;         /* L >= 1: layers in this call's stack              */
+  int32_t batch;              /* B >= 1                                           */
+  int32_t num_q_heads;        /* Hq                                               */
+  int32_t num_kv_heads;       /* Hkv; Hq % Hkv == 0 and 1 <= Hq/Hkv <= 16         */
+  int32_t head_dim;           /* D: 64 or 128                                     */
+  int32_t block_size;         /* must be 16                                       */
+  int32_t max_blocks_per_seq; /* row stride of block_table (>= ceil(max_seq_len/16)) */
+  int32_t max_seq_len;        /* host-known upper bound of seq_lens[]             */
+  int64_t num_blocks;         /* physical blocks per layer in k_cache / v_cache   */
+  int32_t split_blocks;       /* KV blocks per split-K work item: 0 = automatic,
+                                 otherwise an even number in [2, 1024]            */
+  int32_t reserved;           /* must be 0                                        */
+} oda_attn_shape;
+
+/* Inputs of one attention call (host struct holding device pointers). */
+typedef struct {
+  const uint16_t *q;            /* bf16 [L][B][Hq][D]                             */
+  const uint16_t *k_cache;      /* bf16, layout above                             */
+  const uint16_t *v_cache;      /* bf16, layout above                             */
+  const int32_t *block_table;   /* int32 [B][max_blocks_per_seq]: logical block i
+                                   of request b -> physical block id              */
+  const int32_t *seq_lens;      /* int32 [B]: n_b >= 1 attended positions
+                                   0..n_b-1; position n_b-1 is the current token  */
+  const uint16_t *k_cur;        /* NULL: the current token is already in the cache.
+                                   Else bf16 [L][B][Hkv][D]: position n_b-1 is taken
+                                   from here and the cache holds 0..n_b-2          */
+  const uint16_t *v_cur;        /* NULL iff k_cur is NULL                         */
+  float scale;                  /* softmax scale (> 0), usually 1/sqrt(D)         */
+} oda_attn_inputs;
+
+/* Bytes of workspace an attention call with this shape and access set needs.
+ * window == 0 means "no window" (the whole history); window > 0 limits the
+ * recent part to `window` positions.  n_sink >= 0.  (host out) */
+oda_status oda_attn_workspace_size(const oda_attn_shape *shape, int32_t n_sink, int32_t window,
+                                   size_t *bytes);
+
+/* Local decode attention (§2.1 access-set equation; App. A.5 Local path).
+ * For every (layer, request, query head) attends to
+ *     S^L = {j : j < min(n_sink, n)}  U  {j : max(0, n - window) <= j < n}
+ * (0-based, each position once).  window >= 1, n_sink >= 0.  When
+ * n_sink + window >= n the set is the whole history (Local == Full).
+ * Writes out[L][B][Hq][D] and, if lse != NULL, lse[L][B][Hq] for all rows.
+ * workspace: >= oda_attn_workspace_size(shape, n_sink, window) bytes,
+ * 256-byte aligned. */
+oda_status oda_local_decode_attn(const oda_attn_shape *shape, const oda_attn_inputs *in,
+                                 int32_t n_sink, int32_t window, float *out, float *lse,
+                                 void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Recall-head kinds. */
+typedef enum {
+  ODA_HEAD_PAPER = 0, /* App. A.2: RMSNorm->Linear->SiLU towers on h_prev, emb,
+                         h_local; interaction vector; fusion; two pre-RMSNorm
+                         residual SwiGLU blocks; RMSNorm; scalar projection.
+                         d_hidden = tower width dt (SwiGLU hidden 2*dt).       */
+  ODA_HEAD_MLP = 1    /* stand-in: logit = w2 . GELU(W1 h_local + b1) + b2
+                         (exact-erf GELU; sigmoid(logit) is the probability).
+                         d_hidden = h.                                         */
+} oda_head_kind;
+
+/* Recall-gate description (host struct).  params: fp32, packed in this order
+ *   PAPER: for t in (h_prev, emb, h_local): rms_t[d], W_t[dt][d], b_t[dt];
+ *          W_f[dt][9dt], b_f[dt];
+ *          for k in (1,2): rms_k[dt], W_gate_k[2dt][dt], W_up_k[2dt][dt], W_down_k[dt][2dt];
+ *          rms_o[dt], w_o[dt], b_o[1]
+ *   MLP:   W1[h][d], b1[h], w2[h], b2[1]
+ * RMSNorm(x) = x / sqrt(mean(x^2) + rms_eps) * gain. */
+typedef struct {
+  int32_t kind;       /* oda_head_kind                                         */
+  int32_t d_model;    /* d: width of h_prev / emb / h_local, multiple of 4     */
+  int32_t d_hidden;   /* dt (PAPER) or h (MLP), multiple of 4                  */
+  float rms_eps;      /* >= 0; ignored by the MLP                              */
+  const float *params;/* device, oda_gate_param_count() floats                 */
+} oda_gate_desc;
+
+/* Number of fp32 parameters of a head (host out).  For PAPER with d = 2048,
+ * dt = 1024 this is 28,325,889 (App. A.2). */
+oda_status oda_gate_param_count(int32_t kind, int32_t d_model, int32_t d_hidden, int64_t *count);
+
+/* Bytes of workspace oda_recall_gate needs for `batch` requests (host out). */
+oda_status oda_gate_workspace_size(const oda_gate_desc *gate, int32_t batch, size_t *bytes);
+
+/* Recall score and device predicate (§2.1, Alg. 1; App. A.5; App. B.7).
+ *   h_prev, emb, h_local: fp32 [B][d_model] (PAPER reads all three; MLP only
+ *                         h_local; the others may be NULL for MLP)
+ *   tau:      threshold on the raw score (PAPER q_t; MLP pre-sigmoid logit);
+ *             +-INFINITY allowed
+ *   forced:   NULL, or int32 [B] prescribed flags (device-side schedule)
+ *   score:    fp32 [B] out
+ *   flags:    int32 [B] out; 1 iff score > tau or score is nonfinite
+ *             (with `forced`: 1 iff forced[b] != 0 or score is nonfinite)
+ *   work_list, n_work: NULL, or int32 [B] / int32 [1] out: the flagged request
+ *             ids in ascending order and their count
+ *   recall_counter: NULL, or int64 [1]; incremented by the number flagged
+ *             (realised Full-call rate = counter / routed request-steps)
+ * Everything stays on the device; no score is read by the host. */
+oda_status oda_recall_gate(const oda_gate_desc *gate, int32_t batch, const float *h_prev,
+                           const float *emb, const float *h_local, float tau, const int32_t *forced,
+                           float *score, int32_t *flags, int32_t *work_list, int32_t *n_work,
+                           int64_t *recall_counter, void *workspace, size_t workspace_bytes,
+                           hipStream_t stream);
+
+/* Full decode attention in the layers' native configuration (§2.1; App. A.5).
+ * native_window == 0: S^F = all positions 0..n-1 (full-history layers);
+ * native_window  > 0: the last native_window positions (natively
+ * sliding-window layers, which ODA leaves unrestricted).
+ * Request selection:
+ *   work_list != NULL (with n_work != NULL): exactly the listed requests
+ *                       (work_list[0 .. *n_work-1]);
+ *   else flags != NULL: the requests with flags[b] != 0;
+ *   else              : every request.
+ * Only selected requests read KV; only their rows of out (and lse, if not
+ * NULL) are written, so after oda_local_decode_attn + oda_recall_gate the
+ * buffer holds the selected branch per request.
+ * workspace: >= oda_attn_workspace_size(shape, 0, native_window) bytes. */
+oda_status oda_full_decode_attn(const oda_attn_shape *shape, const oda_attn_inputs *in,
+                                int32_t native_window, const int32_t *flags,
+                                const int32_t *work_list, const int32_t *n_work, float *out,
+                                float *lse, void *workspace, size_t workspace_bytes,
+                                hipStream_t stream);
+
+/* Static description of a status code. */
+const char *oda_status_string(oda_status status);
+
+/* Thread-local detail of the last non-OK return on this thread ("" if none). */
+const char *oda_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ODA_H_ */

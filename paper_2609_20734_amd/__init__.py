@@ -1,0 +1,23 @@
+"""On-Demand Attention (ODA) decode-step hot path for AMD MI355X (gfx950).
+
+The product is the C-ABI library ``liboda.so`` (include/oda.h): hand-written
+HIP kernels for Local decode attention, the recall gate with its device
+predicate, and Full decode attention for flagged requests only.  This package
+holds its sources (``csrc/``), its build step (``build.py``), a ctypes
+binding with the same entry-point names (``_lib``), the byte accounting used
+to report bandwidth (``ledger``) and the synthetic workload shapes
+(``workloads``).
+
+The binding is loaded on first use of any entry point; if ``liboda.so`` has
+not been built that raises ImportError (there is no fallback path).
+"""
+_EXPORTS = ("HEAD_MLP", "HEAD_PAPER", "OdaError", "Shape", "attn_workspace_size", "full_decode_attn",
+            "gate_desc", "gate_param_count", "gate_workspace_size", "inputs", "local_decode_attn",
+            "recall_gate", "lib", "prepare_local", "prepare_full", "prepare_gate", "Call")
+
+
+def __getattr__(name):
+    if name in _EXPORTS:
+        from . import _lib
+        return _lib if name == "lib" else getattr(_lib, name)
+    raise AttributeError(name)

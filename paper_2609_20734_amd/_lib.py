@@ -1,0 +1,253 @@
+"""ctypes binding of liboda.so (include/oda.h).
+
+Argument marshalling only: every step of the decode path runs in the HIP
+kernels of the library.  torch tensors supply device memory and the current
+stream.  If the library is not built, importing this module fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+# ODA_LIBRARY may point at another build of the same library (kernel-variant experiments)
+LIB_PATH = os.environ.get("ODA_LIBRARY") or os.path.join(_PKG, "liboda.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_20734_amd.build` "
+                      "(or __graft_entry__.build()) before using the HIP path")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+ODA_OK = 0
+ODA_ERR_NULL = -1
+ODA_ERR_SHAPE = -2
+ODA_ERR_UNSUPPORTED = -3
+ODA_ERR_WORKSPACE = -4
+ODA_ERR_HIP = -5
+
+HEAD_PAPER = 0
+HEAD_MLP = 1
+
+EXPORTED = ("oda_attn_workspace_size", "oda_local_decode_attn", "oda_full_decode_attn",
+            "oda_gate_param_count", "oda_gate_workspace_size", "oda_recall_gate",
+            "oda_status_string", "oda_last_error")
+
+
+class OdaError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"{status_string(status)} ({detail})")
+        self.status = status
+        self.detail = detail
+
+
+class AttnShape(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("batch", ctypes.c_int32),
+                ("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("block_size", ctypes.c_int32),
+                ("max_blocks_per_seq", ctypes.c_int32), ("max_seq_len", ctypes.c_int32),
+                ("num_blocks", ctypes.c_int64), ("split_blocks", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+
+class AttnInputs(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("k_cache", ctypes.c_void_p), ("v_cache", ctypes.c_void_p),
+                ("block_table", ctypes.c_void_p), ("seq_lens", ctypes.c_void_p),
+                ("k_cur", ctypes.c_void_p), ("v_cur", ctypes.c_void_p), ("scale", ctypes.c_float)]
+
+
+class GateDesc(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("d_model", ctypes.c_int32), ("d_hidden", ctypes.c_int32),
+                ("rms_eps", ctypes.c_float), ("params", ctypes.c_void_p)]
+
+
+_P = ctypes.POINTER
+_lib.oda_attn_workspace_size.argtypes = [_P(AttnShape), ctypes.c_int32, ctypes.c_int32, _P(ctypes.c_size_t)]
+_lib.oda_attn_workspace_size.restype = ctypes.c_int
+_lib.oda_local_decode_attn.argtypes = [_P(AttnShape), _P(AttnInputs), ctypes.c_int32, ctypes.c_int32,
+                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                       ctypes.c_void_p]
+_lib.oda_local_decode_attn.restype = ctypes.c_int
+_lib.oda_full_decode_attn.argtypes = [_P(AttnShape), _P(AttnInputs), ctypes.c_int32, ctypes.c_void_p,
+                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+_lib.oda_full_decode_attn.restype = ctypes.c_int
+_lib.oda_gate_param_count.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P(ctypes.c_int64)]
+_lib.oda_gate_param_count.restype = ctypes.c_int
+_lib.oda_gate_workspace_size.argtypes = [_P(GateDesc), ctypes.c_int32, _P(ctypes.c_size_t)]
+_lib.oda_gate_workspace_size.restype = ctypes.c_int
+_lib.oda_recall_gate.argtypes = [_P(GateDesc), ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                 ctypes.c_void_p, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p,
+                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                 ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+_lib.oda_recall_gate.restype = ctypes.c_int
+_lib.oda_status_string.argtypes = [ctypes.c_int]
+_lib.oda_status_string.restype = ctypes.c_char_p
+_lib.oda_last_error.argtypes = []
+_lib.oda_last_error.restype = ctypes.c_char_p
+
+
+def status_string(status: int) -> str:
+    return _lib.oda_status_string(status).decode()
+
+
+def last_error() -> str:
+    return _lib.oda_last_error().decode()
+
+
+def _check(status: int) -> None:
+    if status != ODA_OK:
+        raise OdaError(status, last_error())
+
+
+def _ptr(t) -> int | None:
+    """Device (or host) address of a tensor, None for None; a plain int passes through."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+# ---------------------------------------------------------------------------
+# descriptors
+# ---------------------------------------------------------------------------
+
+@dataclass
+class Shape:
+    num_layers: int
+    batch: int
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    max_blocks_per_seq: int
+    max_seq_len: int
+    num_blocks: int
+    split_blocks: int = 0
+    block_size: int = 16
+
+    def c(self) -> AttnShape:
+        return AttnShape(self.num_layers, self.batch, self.num_q_heads, self.num_kv_heads, self.head_dim,
+                         self.block_size, self.max_blocks_per_seq, self.max_seq_len, self.num_blocks,
+                         self.split_blocks, 0)
+
+
+def inputs(q, k_cache, v_cache, block_table, seq_lens, scale, k_cur=None, v_cur=None) -> AttnInputs:
+    """The C struct of device pointers; it keeps the tensors alive as long as it lives."""
+    s = AttnInputs(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(seq_lens),
+                   _ptr(k_cur), _ptr(v_cur), float(scale))
+    s._keep = (q, k_cache, v_cache, block_table, seq_lens, k_cur, v_cur)
+    return s
+
+
+# ---------------------------------------------------------------------------
+# entry points (same names as the C ABI, without the oda_ prefix)
+# ---------------------------------------------------------------------------
+
+def attn_workspace_size(shape: Shape, n_sink: int, window: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(_lib.oda_attn_workspace_size(ctypes.byref(shape.c()), n_sink, window, ctypes.byref(out)))
+    return out.value
+
+
+def local_decode_attn(shape: Shape, inp: AttnInputs, n_sink: int, window: int, out, lse, workspace,
+                      workspace_bytes: int | None = None, stream=None) -> None:
+    wb = workspace.numel() * workspace.element_size() if workspace_bytes is None and workspace is not None \
+        else (workspace_bytes or 0)
+    _check(_lib.oda_local_decode_attn(ctypes.byref(shape.c()), ctypes.byref(inp), n_sink, window, _ptr(out),
+                                      _ptr(lse), _ptr(workspace), wb, _stream(stream)))
+
+
+def full_decode_attn(shape: Shape, inp: AttnInputs, native_window: int, flags, work_list, n_work, out, lse,
+                     workspace, workspace_bytes: int | None = None, stream=None) -> None:
+    wb = workspace.numel() * workspace.element_size() if workspace_bytes is None and workspace is not None \
+        else (workspace_bytes or 0)
+    _check(_lib.oda_full_decode_attn(ctypes.byref(shape.c()), ctypes.byref(inp), native_window, _ptr(flags),
+                                     _ptr(work_list), _ptr(n_work), _ptr(out), _ptr(lse), _ptr(workspace), wb,
+                                     _stream(stream)))
+
+
+def gate_param_count(kind: int, d_model: int, d_hidden: int) -> int:
+    out = ctypes.c_int64(0)
+    _check(_lib.oda_gate_param_count(kind, d_model, d_hidden, ctypes.byref(out)))
+    return out.value
+
+
+def gate_desc(kind: int, d_model: int, d_hidden: int, params, rms_eps: float = 1e-6) -> GateDesc:
+    """The C gate description; it keeps the parameter tensor alive as long as it lives."""
+    s = GateDesc(kind, d_model, d_hidden, float(rms_eps), _ptr(params))
+    s._keep = params
+    return s
+
+
+def gate_workspace_size(gate: GateDesc, batch: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(_lib.oda_gate_workspace_size(ctypes.byref(gate), batch, ctypes.byref(out)))
+    return out.value
+
+
+def recall_gate(gate: GateDesc, batch: int, h_prev, emb, h_local, tau: float, forced, score, flags, work_list,
+                n_work, recall_counter, workspace, workspace_bytes: int | None = None, stream=None) -> None:
+    wb = workspace.numel() * workspace.element_size() if workspace_bytes is None and workspace is not None \
+        else (workspace_bytes or 0)
+    _check(_lib.oda_recall_gate(ctypes.byref(gate), batch, _ptr(h_prev), _ptr(emb), _ptr(h_local),
+                                float(tau), _ptr(forced), _ptr(score), _ptr(flags), _ptr(work_list),
+                                _ptr(n_work), _ptr(recall_counter), _ptr(workspace), wb, _stream(stream)))
+
+
+# ---------------------------------------------------------------------------
+# pre-marshalled calls (for tight launch loops: no per-call conversion)
+# ---------------------------------------------------------------------------
+
+class Call:
+    """One entry-point call with every argument already converted."""
+    __slots__ = ("fn", "args", "keep")
+
+    def __init__(self, fn, args, keep):
+        self.fn, self.args, self.keep = fn, args, keep
+
+    def __call__(self) -> None:
+        st = self.fn(*self.args)
+        if st != ODA_OK:
+            raise OdaError(st, last_error())
+
+
+def _nbytes(ws, given):
+    if given is not None:
+        return given
+    return 0 if ws is None else ws.numel() * ws.element_size()
+
+
+def prepare_local(shape: Shape, inp: AttnInputs, n_sink: int, window: int, out, lse, workspace,
+                  workspace_bytes: int | None = None, stream=None) -> Call:
+    cs = shape.c()
+    args = (ctypes.byref(cs), ctypes.byref(inp), n_sink, window, _ptr(out), _ptr(lse), _ptr(workspace),
+            _nbytes(workspace, workspace_bytes), _stream(stream))
+    return Call(_lib.oda_local_decode_attn, args, (cs, inp, out, lse, workspace))
+
+
+def prepare_full(shape: Shape, inp: AttnInputs, native_window: int, flags, work_list, n_work, out, lse,
+                 workspace, workspace_bytes: int | None = None, stream=None) -> Call:
+    cs = shape.c()
+    args = (ctypes.byref(cs), ctypes.byref(inp), native_window, _ptr(flags), _ptr(work_list), _ptr(n_work),
+            _ptr(out), _ptr(lse), _ptr(workspace), _nbytes(workspace, workspace_bytes), _stream(stream))
+    return Call(_lib.oda_full_decode_attn, args, (cs, inp, flags, work_list, n_work, out, lse, workspace))
+
+
+def prepare_gate(gate: GateDesc, batch: int, h_prev, emb, h_local, tau: float, forced, score, flags, work_list,
+                 n_work, recall_counter, workspace, workspace_bytes: int | None = None, stream=None) -> Call:
+    args = (ctypes.byref(gate), batch, _ptr(h_prev), _ptr(emb), _ptr(h_local), float(tau), _ptr(forced),
+            _ptr(score), _ptr(flags), _ptr(work_list), _ptr(n_work), _ptr(recall_counter), _ptr(workspace),
+            _nbytes(workspace, workspace_bytes), _stream(stream))
+    return Call(_lib.oda_recall_gate, args, (gate, h_prev, emb, h_local, forced, score, flags, work_list, n_work,
+                                            recall_counter, workspace))

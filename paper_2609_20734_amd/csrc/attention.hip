@@ -1,0 +1,761 @@
+// Decode attention over a paged bf16 KV cache for gfx950 (CDNA4):
+// oda_local_decode_attn (Local access set) and oda_full_decode_attn (native
+// access set, flagged requests only).  Both run the same kernels:
+//
+//   split  -- one workgroup of W wavefronts per work item (layer, request, KV
+//             head, split).  Each wavefront streams a contiguous run of the
+//             item's KV blocks, computes the G query heads' scores with
+//             v_mfma_f32_16x16x32_bf16 (K tile x Q^T), keeps an online
+//             softmax and accumulates P V with the same MFMA (P split into a
+//             bf16 high and low part so the product keeps fp32 accuracy).
+//             The wavefronts then combine their (m, l, o) through LDS.  If the
+//             item covers the request's whole access set the workgroup writes
+//             out / lse directly (adding the uncommitted current candidate);
+//             otherwise it writes an unnormalised partial.
+//   merge  -- only when some request needs several splits: one workgroup per
+//             (layer, request, KV head) combines the partials with stable
+//             softmax rescaling (plus the candidate) and writes out / lse.
+// This is the split-phase / combine-phase structure the paper's Local path
+// uses (App. A.5), applied to both branches.
+//
+// Register layouts of one 16x16x32 MFMA (lane l, h = l % 16, j = l / 16):
+//   A (16 x 32): row h, k = 8j..8j+7      B (32 x 16): column h, k = 8j..8j+7
+//   C (16 x 16): column h, rows 4j..4j+3
+// The cache layouts are chosen so every operand is one aligned global load:
+//   K block [D/8][16][8]: 16 bytes at ((kk*4 + j)*16 + h)*8 is key h, dims
+//     32kk + 8j .. +7  ->  the A operand of S^T = K Q^T (rows = positions);
+//   V block [D][16]: 8 bytes at d*16 + 4j are positions 4j..4j+3 of dim d ->
+//     two blocks give the B operand of O = P V (k = 8 positions, columns = dims),
+//     matching the C layout of S^T (lane holds positions 4j..4j+3 of each tile).
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <cmath>
+
+#include "oda.h"
+#include "oda_internal.h"
+
+#ifndef ODA_KV_NONTEMPORAL
+#define ODA_KV_NONTEMPORAL 1
+#endif
+#ifndef ODA_SPLIT_PREFETCH
+#define ODA_SPLIT_PREFETCH 0
+#endif
+#ifndef ODA_SPLIT_WAVES
+#define ODA_SPLIT_WAVES 8
+#endif
+#ifndef ODA_TARGET_GROUPS
+#define ODA_TARGET_GROUPS 256
+#endif
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kBlock = 16;            // positions per KV block
+constexpr int kMaxGroup = 16;         // query heads per KV head held by one MFMA tile
+constexpr int kWaves = ODA_SPLIT_WAVES;   // wavefronts per split workgroup
+constexpr int kMergeThreads = 256;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+enum Select { kSelAll = 0, kSelFlags = 1, kSelList = 2 };
+
+struct AttnArgs {
+  const uint16_t* q;
+  const uint16_t* k_cache;
+  const uint16_t* v_cache;
+  const int32_t* block_table;
+  const int32_t* seq_lens;
+  const uint16_t* k_cur;
+  const uint16_t* v_cur;
+  const int32_t* flags;
+  const int32_t* work_list;
+  const int32_t* n_work;
+  float* out;
+  float* lse;
+  float* part_o;     // [L][B][Hkv][max_splits][G][D]
+  float* part_ml;    // [L][B][Hkv][max_splits][G][2]  (m in log2 units, l)
+  int64_t kv_layer_stride;  // elements between layers of k_cache / v_cache
+  int32_t L, B, Hq, Hkv, G, MB;
+  int32_t n_sink, window;   // window <= 0: no window
+  int32_t has_cur;
+  int32_t bps, max_splits;
+  int32_t select;
+  float scale_log2;         // scale * log2(e)
+};
+
+// Positions of one request attended through the cache, as block ranges.
+//   A = [0, a_end)          the sink part
+//   R = [r_start, nc)       the recent part (nc = cache end: n, or n-1 when
+//                           the current token comes from k_cur)
+// Blocks visited: [0, ab_end) then [rb_lo, rb_hi); a block holding both A and
+// R positions is visited once (in the first range).  "Virtual" block v counts
+// the visited blocks in that order.
+struct Geometry {
+  int a_end, r_start, nc, ab_end, rb_lo, rb_hi, nvb;
+};
+
+__device__ __forceinline__ Geometry geometry(int n, int n_sink, int window, int has_cur) {
+  Geometry g;
+  g.nc = n - has_cur;
+  const int sink_end = min(n_sink, n);
+  g.a_end = min(sink_end, g.nc);
+  const int win_start = window > 0 ? max(0, n - window) : 0;
+  g.r_start = max(win_start, sink_end);
+  g.ab_end = (g.a_end + kBlock - 1) / kBlock;
+  if (g.r_start < g.nc) {
+    g.rb_lo = max(g.r_start / kBlock, g.ab_end);
+    g.rb_hi = (g.nc + kBlock - 1) / kBlock;
+  } else {
+    g.rb_lo = g.rb_hi = 0;
+  }
+  g.nvb = g.ab_end + (g.rb_hi - g.rb_lo);
+  return g;
+}
+
+__device__ __forceinline__ int logical_block(const Geometry& g, int v) {
+  return v < g.ab_end ? v : g.rb_lo + (v - g.ab_end);
+}
+
+__device__ __forceinline__ bool in_set(const Geometry& g, int p) {
+  return p < g.a_end || (p >= g.r_start && p < g.nc);
+}
+
+// All 16 positions of logical block lb attended?
+__device__ __forceinline__ bool block_full(const Geometry& g, int lb) {
+  const int p0 = lb * kBlock, p1 = p0 + kBlock;
+  return p1 <= g.a_end || (p0 >= g.r_start && p1 <= g.nc);
+}
+
+// Map a slot of the request dimension to a request id; false if the slot has
+// no selected request.
+__device__ __forceinline__ bool resolve_request(const AttnArgs& a, int slot, int& b) {
+  if (a.select == kSelList) {
+    if (slot >= a.n_work[0]) return false;
+    b = a.work_list[slot];
+    return true;
+  }
+  b = slot;
+  if (a.select == kSelFlags) return a.flags[slot] != 0;
+  return true;
+}
+
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+__device__ __forceinline__ bf16x8 load16(const uint16_t* p) {
+  return *reinterpret_cast<const bf16x8*>(p);
+}
+// KV is read once per call: stream it with nontemporal loads.
+__device__ __forceinline__ bf16x8 stream16(const uint16_t* p) {
+#if ODA_KV_NONTEMPORAL
+  return __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(p));
+#else
+  return *reinterpret_cast<const bf16x8*>(p);
+#endif
+}
+__device__ __forceinline__ u32x2 stream8(const uint16_t* p) {
+#if ODA_KV_NONTEMPORAL
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+#else
+  return *reinterpret_cast<const u32x2*>(p);
+#endif
+}
+__device__ __forceinline__ bf16x8 cat(u32x2 lo, u32x2 hi) {
+  u32x4 t = {lo.x, lo.y, hi.x, hi.y};
+  return __builtin_bit_cast(bf16x8, t);
+}
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float bf16_to_float(uint16_t x) {
+  return __builtin_bit_cast(float, (uint32_t)x << 16);
+}
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int s = 32; s >= 1; s >>= 1) x += __shfl_xor(x, s);
+  return x;
+}
+
+// Keep the 16-bit lanes of a 4 x bf16 pack whose position is attended.
+__device__ __forceinline__ u32x2 mask_pack(u32x2 v, bool m0, bool m1, bool m2, bool m3) {
+  const uint32_t w0 = (m0 ? 0x0000FFFFu : 0u) | (m1 ? 0xFFFF0000u : 0u);
+  const uint32_t w1 = (m2 ? 0x0000FFFFu : 0u) | (m3 ? 0xFFFF0000u : 0u);
+  u32x2 r = {v.x & w0, v.y & w1};
+  return r;
+}
+
+// Registers of one pair of KV blocks (32 positions) in MFMA operand layout.
+template <int D>
+struct PairTile {
+  bf16x8 k0[D / 32], k1[D / 32];
+  u32x2 v0[D / 16], v1[D / 16];
+};
+
+// One wavefront's run of blocks: virtual blocks [v_lo, v_hi) of its request;
+// lane i of the table register holds the physical block of virtual block
+// v_lo + 64c + i for the current chunk c of 64 blocks.
+struct Run {
+  Geometry geo;
+  const uint16_t* kbase;
+  const uint16_t* vbase;
+  const int32_t* bt;
+  int64_t blk_stride;
+  int v_lo, v_hi;
+};
+
+__device__ __forceinline__ int table_chunk(const Run& r, int chunk, int lane) {
+  const int v = r.v_lo + chunk * 64 + lane;
+  return v < r.v_hi ? r.bt[logical_block(r.geo, v)] : 0;
+}
+
+template <int D>
+__device__ __forceinline__ void load_pair(PairTile<D>& t, const Run& r, int v, int tbl, int lane) {
+  constexpr int KK = D / 32, NT = D / 16;
+  const int h16 = lane & 15, j = lane >> 4;
+  const int i0 = (v - r.v_lo) & 63;
+  const int64_t pb0 = __builtin_amdgcn_readlane(tbl, i0);
+  // an odd tail reuses block 0 for the second tile; all its positions are masked
+  const int64_t pb1 = (v + 1 < r.v_hi) ? __builtin_amdgcn_readlane(tbl, i0 + 1) : pb0;
+  const uint16_t* k0 = r.kbase + pb0 * r.blk_stride;
+  const uint16_t* k1 = r.kbase + pb1 * r.blk_stride;
+  const uint16_t* v0 = r.vbase + pb0 * r.blk_stride;
+  const uint16_t* v1 = r.vbase + pb1 * r.blk_stride;
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    t.k0[kk] = stream16(k0 + (kk * 64 + lane) * 8);
+    t.k1[kk] = stream16(k1 + (kk * 64 + lane) * 8);
+  }
+#pragma unroll
+  for (int n = 0; n < NT; ++n) {
+    const int d = 16 * n + h16;
+    t.v0[n] = stream8(v0 + d * kBlock + 4 * j);
+    t.v1[n] = stream8(v1 + d * kBlock + 4 * j);
+  }
+}
+
+// One pair of blocks: S^T on MFMA, online softmax of head h16, O += P V on MFMA.
+template <int D>
+__device__ __forceinline__ void consume_pair(PairTile<D>& t, const Run& r, int v, int lane, const bf16x8* qf,
+                                             float scale_log2, f32x4* o, float& m_run, float& l_run) {
+  constexpr int KK = D / 32, NT = D / 16;
+  const int j = lane >> 4;
+  const bool has1 = (v + 1) < r.v_hi;
+  const int lb0 = logical_block(r.geo, v);
+  const int lb1 = has1 ? logical_block(r.geo, v + 1) : lb0;
+
+  f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(t.k0[kk], qf[kk], s0, 0, 0, 0);
+    s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(t.k1[kk], qf[kk], s1, 0, 0, 0);
+  }
+  float sc[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    sc[i] = s0[i] * scale_log2;
+    sc[4 + i] = s1[i] * scale_log2;
+  }
+  const bool full0 = block_full(r.geo, lb0);
+  const bool full1 = has1 && block_full(r.geo, lb1);
+  if (!(full0 && full1)) {
+    bool m[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      m[i] = in_set(r.geo, lb0 * kBlock + 4 * j + i);
+      m[4 + i] = has1 && in_set(r.geo, lb1 * kBlock + 4 * j + i);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) sc[i] = m[i] ? sc[i] : -INFINITY;
+    // unattended slots may hold anything (even NaN): zero them so 0 * V stays 0
+#pragma unroll
+    for (int n = 0; n < NT; ++n) {
+      t.v0[n] = mask_pack(t.v0[n], m[0], m[1], m[2], m[3]);
+      t.v1[n] = mask_pack(t.v1[n], m[4], m[5], m[6], m[7]);
+    }
+  }
+
+  // online softmax for head h16 (its 32 positions are spread over lanes h16 + 16j)
+  float mx = sc[0];
+#pragma unroll
+  for (int i = 1; i < 8; ++i) mx = fmaxf(mx, sc[i]);
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const float m_new = fmaxf(m_run, mx);
+  const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+  const float alpha = exp2_fast(m_run - m_use);
+  m_run = m_new;
+  float p[8];
+  float psum = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    p[i] = exp2_fast(sc[i] - m_use);
+    psum += p[i];
+  }
+  l_run = l_run * alpha + psum;
+
+  // rescale O rows (heads 4j..4j+3) by their heads' alpha, when any changed
+  if (__any(alpha != 1.f)) {
+    float al[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) al[i] = __shfl(alpha, 4 * j + i);
+#pragma unroll
+    for (int n = 0; n < NT; ++n) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[n][i] *= al[i];
+    }
+  }
+
+  // P as the A operand (row = head h16, k = its 8 positions), split hi + lo
+  bf16x8 phi, plo;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const __bf16 h = (__bf16)p[i];
+    phi[i] = h;
+    plo[i] = (__bf16)(p[i] - (float)h);
+  }
+#pragma unroll
+  for (int n = 0; n < NT; ++n) {
+    const bf16x8 vf = cat(t.v0[n], t.v1[n]);
+    o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(phi, vf, o[n], 0, 0, 0);
+    o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(plo, vf, o[n], 0, 0, 0);
+  }
+}
+
+// Shared memory of the split workgroup (dynamic): per wavefront m[16], l[16]
+// and o[G][D]; then the candidate logits zc[16].
+__host__ __device__ constexpr size_t split_lds_floats(int G, int D) {
+  return (size_t)kWaves * 32 + (size_t)kWaves * G * D + 16;
+}
+
+template <int D>
+__global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
+void attn_split_kernel(AttnArgs a) {
+  constexpr int KK = D / 32;   // MFMA k-steps for q.k
+  constexpr int NT = D / 16;   // 16-dim output tiles
+  extern __shared__ float smem[];
+  const int lane = threadIdx.x & 63;
+  const int wave = uniform(threadIdx.x >> 6);
+  const int h16 = lane & 15;
+  const int j = lane >> 4;
+
+  int64_t item = blockIdx.x;
+  const int split = (int)(item % a.max_splits);
+  item /= a.max_splits;
+  const int g = (int)(item % a.Hkv);
+  item /= a.Hkv;
+  const int slot = (int)(item % a.B);
+  const int l = (int)(item / a.B);
+  if (l >= a.L) return;
+  int b;
+  if (!resolve_request(a, slot, b)) return;
+  b = uniform(b);
+  const int n = uniform(a.seq_lens[b]);
+  Run r;
+  r.geo = geometry(n, a.n_sink, a.window, a.has_cur);
+  // (nvb = 0 happens only with the candidate as the sole position: one item, no blocks)
+  const int nsplit = max(1, (r.geo.nvb + a.bps - 1) / a.bps);
+  if (split >= nsplit) return;   // uniform over the workgroup: no barrier is skipped by part of it
+  const int G = a.G;
+
+  // this wavefront's run: a contiguous share of the split's pairs
+  const int v_begin = split * a.bps;
+  const int v_end = min(r.geo.nvb, v_begin + a.bps);
+  const int pairs = (v_end - v_begin + 1) >> 1;
+  const int per_wave = (pairs + kWaves - 1) / kWaves;
+  r.v_lo = min(v_end, v_begin + 2 * per_wave * wave);
+  r.v_hi = min(v_end, r.v_lo + 2 * per_wave);
+
+  const int64_t head_elems = (int64_t)kBlock * D;
+  r.kbase = a.k_cache + (int64_t)l * a.kv_layer_stride + (int64_t)g * head_elems;
+  r.vbase = a.v_cache + (int64_t)l * a.kv_layer_stride + (int64_t)g * head_elems;
+  r.blk_stride = (int64_t)a.Hkv * head_elems;
+  r.bt = a.block_table + (int64_t)b * a.MB;
+
+  f32x4 o[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY;  // running max (log2 units) of head h16
+  float l_run = 0.f;        // this lane's share of the running exp-sum
+
+  if (r.v_lo < r.v_hi) {
+    // Q^T as the B operand: column = query head h16 of this KV head's group.
+    bf16x8 qf[KK];
+    const uint16_t* qrow = a.q + (((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G + h16) * D;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) qf[kk] = (h16 < G) ? load16(qrow + 32 * kk + 8 * j) : bf16x8{};
+
+    int tbl = table_chunk(r, 0, lane);
+    int tbl_next = table_chunk(r, 1, lane);
+#if ODA_SPLIT_PREFETCH
+    PairTile<D> ta, tb;
+    load_pair<D>(ta, r, r.v_lo, tbl, lane);
+    for (int v = r.v_lo; v < r.v_hi; v += 4) {
+      const bool more1 = v + 2 < r.v_hi;
+      if (more1) {
+        if (((v + 2 - r.v_lo) & 63) == 0) {   // entering the next 64-block chunk of the table
+          tbl = tbl_next;
+          tbl_next = table_chunk(r, ((v + 2 - r.v_lo) >> 6) + 1, lane);
+        }
+        load_pair<D>(tb, r, v + 2, tbl, lane);
+      }
+      consume_pair<D>(ta, r, v, lane, qf, a.scale_log2, o, m_run, l_run);
+      if (!more1) break;
+      if (v + 4 < r.v_hi) {
+        if (((v + 4 - r.v_lo) & 63) == 0) {
+          tbl = tbl_next;
+          tbl_next = table_chunk(r, ((v + 4 - r.v_lo) >> 6) + 1, lane);
+        }
+        load_pair<D>(ta, r, v + 4, tbl, lane);
+      }
+      consume_pair<D>(tb, r, v + 2, lane, qf, a.scale_log2, o, m_run, l_run);
+    }
+#else
+    for (int v = r.v_lo; v < r.v_hi; v += 2) {
+      if (v > r.v_lo && ((v - r.v_lo) & 63) == 0) {
+        tbl = tbl_next;
+        tbl_next = table_chunk(r, ((v - r.v_lo) >> 6) + 1, lane);
+      }
+      PairTile<D> ta;
+      load_pair<D>(ta, r, v, tbl, lane);
+      consume_pair<D>(ta, r, v, lane, qf, a.scale_log2, o, m_run, l_run);
+    }
+#endif
+    l_run += __shfl_xor(l_run, 16);
+    l_run += __shfl_xor(l_run, 32);
+  }
+
+  // combine the wavefronts through LDS
+  float* sm_m = smem;                        // [kWaves][16]
+  float* sm_l = smem + kWaves * 16;          // [kWaves][16]
+  float* sm_o = smem + kWaves * 32;          // [kWaves][G][D]
+  float* sm_zc = sm_o + kWaves * G * D;      // [16]
+  if (j == 0) {
+    sm_m[wave * 16 + h16] = m_run;
+    sm_l[wave * 16 + h16] = l_run;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int hh = 4 * j + i;
+    if (hh < G) {
+      float* dst = sm_o + ((int64_t)wave * G + hh) * D + h16;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) dst[16 * t] = o[t][i];
+    }
+  }
+  const bool finalize = (nsplit == 1);
+  const int64_t qoff = (((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G) * D;
+  const int64_t coff = (((int64_t)l * a.B + b) * a.Hkv + g) * D;
+  if (finalize && a.has_cur && wave == 0) {
+    // candidate logits of the G heads (log2 units)
+    constexpr int PD = D / 64;
+    float kc[PD];
+#pragma unroll
+    for (int e = 0; e < PD; ++e) kc[e] = bf16_to_float(a.k_cur[coff + lane * PD + e]);
+    for (int hh = 0; hh < G; ++hh) {
+      float dot = 0.f;
+#pragma unroll
+      for (int e = 0; e < PD; ++e) dot += bf16_to_float(a.q[qoff + hh * D + lane * PD + e]) * kc[e];
+      dot = wave_sum(dot) * a.scale_log2;
+      if (lane == 0) sm_zc[hh] = dot;
+    }
+  }
+  __syncthreads();
+
+  const int64_t pidx = (((int64_t)l * a.B + b) * a.Hkv + g) * a.max_splits + split;
+  for (int e = threadIdx.x; e < G * D; e += kWaves * 64) {
+    const int hh = e / D, d = e - hh * D;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sm_m[w * 16 + hh]);
+    const float Mu = (M == -INFINITY) ? 0.f : M;
+    float acc = 0.f, lam = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float s = exp2_fast(sm_m[w * 16 + hh] - Mu);
+      acc += s * sm_o[((int64_t)w * G + hh) * D + d];
+      lam += s * sm_l[w * 16 + hh];
+    }
+    if (finalize) {
+      if (a.has_cur) {
+        const float z = sm_zc[hh];
+        const float M2 = fmaxf(M, z);
+        const float s_old = exp2_fast(M - M2), s_cur = exp2_fast(z - M2);
+        acc = acc * s_old + s_cur * bf16_to_float(a.v_cur[coff + d]);
+        lam = lam * s_old + s_cur;
+        M = M2;
+      }
+      a.out[qoff + e] = acc / lam;
+      if (d == 0 && a.lse != nullptr)
+        a.lse[((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G + hh] = (M + __log2f(lam)) * kLn2;
+    } else {
+      a.part_o[pidx * G * D + e] = acc;
+      if (d == 0) {
+        a.part_ml[(pidx * G + hh) * 2 + 0] = M;
+        a.part_ml[(pidx * G + hh) * 2 + 1] = lam;
+      }
+    }
+  }
+}
+
+// One workgroup per (layer, request slot, KV head) whose request has several
+// splits: thread e owns entries e, e + 256, ... of the [G][D] block.
+template <int D>
+__global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(AttnArgs a) {
+  __shared__ float sm_zc[kMaxGroup];
+  int64_t unit = blockIdx.x;
+  const int g = (int)(unit % a.Hkv);
+  unit /= a.Hkv;
+  const int slot = (int)(unit % a.B);
+  const int l = (int)(unit / a.B);
+  if (l >= a.L) return;
+  int b;
+  if (!resolve_request(a, slot, b)) return;
+  b = uniform(b);
+  const int n = uniform(a.seq_lens[b]);
+  const Geometry geo = geometry(n, a.n_sink, a.window, a.has_cur);
+  const int nsplit = max(1, (geo.nvb + a.bps - 1) / a.bps);
+  if (nsplit <= 1) return;   // finalized by the split kernel
+  const int G = a.G;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t pbase = (((int64_t)l * a.B + b) * a.Hkv + g) * a.max_splits;
+  const float* ml = a.part_ml + pbase * G * 2;
+  const float* po = a.part_o + pbase * G * D;
+  const int64_t qoff = (((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G) * D;
+  const int64_t coff = (((int64_t)l * a.B + b) * a.Hkv + g) * D;
+
+  if (a.has_cur) {
+    constexpr int PD = D / 64;
+    float kc[PD];
+#pragma unroll
+    for (int e = 0; e < PD; ++e) kc[e] = bf16_to_float(a.k_cur[coff + lane * PD + e]);
+    for (int hh = wave; hh < G; hh += kMergeThreads / 64) {
+      float dot = 0.f;
+#pragma unroll
+      for (int e = 0; e < PD; ++e) dot += bf16_to_float(a.q[qoff + hh * D + lane * PD + e]) * kc[e];
+      dot = wave_sum(dot) * a.scale_log2;
+      if (lane == 0) sm_zc[hh] = dot;
+    }
+    __syncthreads();
+  }
+
+  for (int e = threadIdx.x; e < G * D; e += kMergeThreads) {
+    const int hh = e / D, d = e - hh * D;
+    float M = a.has_cur ? sm_zc[hh] : -INFINITY;
+    for (int s = 0; s < nsplit; ++s) M = fmaxf(M, ml[(s * G + hh) * 2]);
+    float acc = 0.f, lam = 0.f;
+#pragma unroll 4
+    for (int s = 0; s < nsplit; ++s) {
+      const float w = exp2_fast(ml[(s * G + hh) * 2] - M);
+      acc += w * __builtin_nontemporal_load(po + ((int64_t)s * G + hh) * D + d);
+      lam += w * ml[(s * G + hh) * 2 + 1];
+    }
+    if (a.has_cur) {
+      const float w = exp2_fast(sm_zc[hh] - M);
+      acc += w * bf16_to_float(a.v_cur[coff + d]);
+      lam += w;
+    }
+    a.out[qoff + e] = acc / lam;
+    if (d == 0 && a.lse != nullptr)
+      a.lse[((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G + hh] = (M + __log2f(lam)) * kLn2;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+
+struct Plan {
+  int nvb_max;
+  int bps;
+  int max_splits;
+  size_t off_ml;
+  size_t bytes;
+};
+
+oda_status check_shape(const oda_attn_shape* s) {
+  if (s == nullptr) return oda::fail(ODA_ERR_NULL, "shape is NULL");
+  if (s->num_layers < 1 || s->batch < 1 || s->num_q_heads < 1 || s->num_kv_heads < 1)
+    return oda::fail(ODA_ERR_SHAPE, "num_layers, batch, num_q_heads, num_kv_heads must be >= 1");
+  if (s->num_q_heads % s->num_kv_heads != 0)
+    return oda::fail(ODA_ERR_SHAPE, "num_q_heads (%d) must be a multiple of num_kv_heads (%d)",
+                     s->num_q_heads, s->num_kv_heads);
+  if (s->num_q_heads / s->num_kv_heads > kMaxGroup)
+    return oda::fail(ODA_ERR_UNSUPPORTED, "GQA group size %d > %d", s->num_q_heads / s->num_kv_heads,
+                     kMaxGroup);
+  if (s->head_dim != 64 && s->head_dim != 128)
+    return oda::fail(ODA_ERR_UNSUPPORTED, "head_dim %d not in {64, 128}", s->head_dim);
+  if (s->block_size != kBlock) return oda::fail(ODA_ERR_UNSUPPORTED, "block_size %d != 16", s->block_size);
+  if (s->max_seq_len < 1) return oda::fail(ODA_ERR_SHAPE, "max_seq_len must be >= 1");
+  if ((int64_t)s->max_blocks_per_seq < oda::ceil_div(s->max_seq_len, kBlock))
+    return oda::fail(ODA_ERR_SHAPE, "max_blocks_per_seq %d < ceil(max_seq_len / 16)", s->max_blocks_per_seq);
+  if (s->num_blocks < 1) return oda::fail(ODA_ERR_SHAPE, "num_blocks must be >= 1");
+  if (s->split_blocks != 0 && (s->split_blocks < 2 || (s->split_blocks & 1)))
+    return oda::fail(ODA_ERR_SHAPE, "split_blocks %d: 0 or an even number >= 2", s->split_blocks);
+  if (s->reserved != 0) return oda::fail(ODA_ERR_SHAPE, "reserved must be 0");
+  return ODA_OK;
+}
+
+// Work decomposition.  One workgroup per (layer, request, KV head, split);
+// the automatic plan splits only as much as needed to give the GPU about
+// ODA_TARGET_GROUPS workgroups (one per CU), so most calls finish in the split
+// kernel and skip the merge.
+void make_plan(const oda_attn_shape* s, int n_sink, int window, Plan* p) {
+  const int64_t total_blocks = oda::ceil_div(s->max_seq_len, kBlock);
+  int64_t nvb = total_blocks;
+  if (window > 0) {
+    const int64_t sink_blocks = oda::ceil_div(std::min<int64_t>(n_sink, s->max_seq_len), kBlock);
+    nvb = std::min<int64_t>(total_blocks, sink_blocks + oda::ceil_div(window, kBlock) + 1);
+  }
+  const int64_t units = (int64_t)s->num_layers * s->batch * s->num_kv_heads;
+  int64_t bps = s->split_blocks;
+  if (bps == 0) {
+    const int64_t want = oda::ceil_div(ODA_TARGET_GROUPS, units);
+    // at least 4 blocks per wavefront
+    const int64_t max_split = std::max<int64_t>(1, nvb / (4 * kWaves));
+    const int64_t nsplit = std::max<int64_t>(1, std::min(want, max_split));
+    bps = oda::round_up(oda::ceil_div(nvb, nsplit), 2);
+  }
+  p->nvb_max = (int)nvb;
+  p->bps = (int)std::min<int64_t>(bps, 1 << 30);
+  p->max_splits = (int)oda::ceil_div(nvb, bps);
+  if (p->max_splits <= 1) {
+    p->off_ml = 0;
+    p->bytes = 0;
+    return;
+  }
+  const int64_t G = s->num_q_heads / s->num_kv_heads;
+  const int64_t parts = units * p->max_splits * G;
+  const int64_t o_bytes = oda::round_up(parts * s->head_dim * 4, 256);
+  const int64_t ml_bytes = oda::round_up(parts * 2 * 4, 256);
+  p->off_ml = (size_t)o_bytes;
+  p->bytes = (size_t)(o_bytes + ml_bytes);
+}
+
+oda_status check_inputs(const oda_attn_inputs* in, const float* out) {
+  if (in == nullptr) return oda::fail(ODA_ERR_NULL, "inputs is NULL");
+  if (!in->q || !in->k_cache || !in->v_cache || !in->block_table || !in->seq_lens || !out)
+    return oda::fail(ODA_ERR_NULL, "q, k_cache, v_cache, block_table, seq_lens and out are required");
+  if ((in->k_cur == nullptr) != (in->v_cur == nullptr))
+    return oda::fail(ODA_ERR_NULL, "k_cur and v_cur must both be NULL or both be set");
+  if (!oda::aligned(in->q, 16) || !oda::aligned(in->k_cache, 16) || !oda::aligned(in->v_cache, 16) ||
+      !oda::aligned(out, 16) || (in->k_cur && (!oda::aligned(in->k_cur, 16) || !oda::aligned(in->v_cur, 16))))
+    return oda::fail(ODA_ERR_SHAPE, "q, caches, k_cur, v_cur and out must be 16-byte aligned");
+  if (!(in->scale > 0.f) || !std::isfinite(in->scale))
+    return oda::fail(ODA_ERR_SHAPE, "scale must be finite and > 0");
+  return ODA_OK;
+}
+
+template <int D>
+oda_status launch(const AttnArgs& args, const Plan& plan, hipStream_t stream) {
+  const int64_t units = (int64_t)args.L * args.B * args.Hkv;
+  const int64_t items = units * plan.max_splits;
+  if (items > 0x7fffffffLL) return oda::fail(ODA_ERR_SHAPE, "grid too large (%lld work items)", (long long)items);
+  const size_t lds = split_lds_floats(args.G, D) * sizeof(float);
+  static bool lds_raised = false;
+  if (!lds_raised) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(attn_split_kernel<D>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)(split_lds_floats(kMaxGroup, D) * 4));
+    lds_raised = true;
+  }
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(attn_split_kernel<D>, dim3((unsigned)items), dim3(kWaves * 64), lds, stream, args);
+  if (plan.max_splits > 1)
+    hipLaunchKernelGGL(attn_merge_kernel<D>, dim3((unsigned)units), dim3(kMergeThreads), 0, stream, args);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return oda::fail(ODA_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ODA_OK;
+}
+
+oda_status run_attention(const oda_attn_shape* s, const oda_attn_inputs* in, int n_sink, int window,
+                         int select, const int32_t* flags, const int32_t* work_list, const int32_t* n_work,
+                         float* out, float* lse, void* ws, size_t ws_bytes, hipStream_t stream) {
+  Plan plan;
+  make_plan(s, n_sink, window, &plan);
+  if (plan.bytes > 0) {
+    if (ws == nullptr) return oda::fail(ODA_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", plan.bytes);
+    if (ws_bytes < plan.bytes)
+      return oda::fail(ODA_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, plan.bytes);
+    if (!oda::aligned(ws, 256)) return oda::fail(ODA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  }
+  AttnArgs a;
+  a.q = in->q;
+  a.k_cache = in->k_cache;
+  a.v_cache = in->v_cache;
+  a.block_table = in->block_table;
+  a.seq_lens = in->seq_lens;
+  a.k_cur = in->k_cur;
+  a.v_cur = in->v_cur;
+  a.flags = flags;
+  a.work_list = work_list;
+  a.n_work = n_work;
+  a.out = out;
+  a.lse = lse;
+  a.part_o = static_cast<float*>(ws);
+  a.part_ml = plan.bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + plan.off_ml) : nullptr;
+  a.kv_layer_stride = s->num_blocks * s->num_kv_heads * kBlock * s->head_dim;
+  a.L = s->num_layers;
+  a.B = s->batch;
+  a.Hq = s->num_q_heads;
+  a.Hkv = s->num_kv_heads;
+  a.G = s->num_q_heads / s->num_kv_heads;
+  a.MB = s->max_blocks_per_seq;
+  a.n_sink = n_sink;
+  a.window = window;
+  a.has_cur = in->k_cur != nullptr;
+  a.bps = plan.bps;
+  a.max_splits = plan.max_splits;
+  a.select = select;
+  a.scale_log2 = in->scale * kLog2e;
+  oda_status st = s->head_dim == 128 ? launch<128>(a, plan, stream) : launch<64>(a, plan, stream);
+  if (st != ODA_OK) return st;
+  return oda::ok();
+}
+
+}  // namespace
+
+extern "C" oda_status oda_attn_workspace_size(const oda_attn_shape* shape, int32_t n_sink, int32_t window,
+                                              size_t* bytes) {
+  oda_status st = check_shape(shape);
+  if (st != ODA_OK) return st;
+  if (bytes == nullptr) return oda::fail(ODA_ERR_NULL, "bytes is NULL");
+  if (n_sink < 0 || window < 0) return oda::fail(ODA_ERR_SHAPE, "n_sink and window must be >= 0");
+  Plan plan;
+  make_plan(shape, n_sink, window, &plan);
+  *bytes = plan.bytes;
+  return oda::ok();
+}
+
+extern "C" oda_status oda_local_decode_attn(const oda_attn_shape* shape, const oda_attn_inputs* in,
+                                           int32_t n_sink, int32_t window, float* out, float* lse,
+                                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  oda_status st = check_shape(shape);
+  if (st != ODA_OK) return st;
+  st = check_inputs(in, out);
+  if (st != ODA_OK) return st;
+  if (n_sink < 0) return oda::fail(ODA_ERR_SHAPE, "n_sink must be >= 0");
+  if (window < 1) return oda::fail(ODA_ERR_SHAPE, "window must be >= 1 for Local attention");
+  return run_attention(shape, in, n_sink, window, kSelAll, nullptr, nullptr, nullptr, out, lse, workspace,
+                       workspace_bytes, stream);
+}
+
+extern "C" oda_status oda_full_decode_attn(const oda_attn_shape* shape, const oda_attn_inputs* in,
+                                          int32_t native_window, const int32_t* flags,
+                                          const int32_t* work_list, const int32_t* n_work, float* out,
+                                          float* lse, void* workspace, size_t workspace_bytes,
+                                          hipStream_t stream) {
+  oda_status st = check_shape(shape);
+  if (st != ODA_OK) return st;
+  st = check_inputs(in, out);
+  if (st != ODA_OK) return st;
+  if (native_window < 0) return oda::fail(ODA_ERR_SHAPE, "native_window must be >= 0");
+  if ((work_list == nullptr) != (n_work == nullptr))
+    return oda::fail(ODA_ERR_NULL, "work_list and n_work must both be NULL or both be set");
+  const int select = work_list ? kSelList : (flags ? kSelFlags : kSelAll);
+  return run_attention(shape, in, 0, native_window, select, flags, work_list, n_work, out, lse, workspace,
+                       workspace_bytes, stream);
+}

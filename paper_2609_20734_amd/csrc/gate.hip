@@ -1,0 +1,463 @@
+// Recall gate on gfx950: the recall score (head of App. A.2, or the two-layer
+// MLP stand-in) and the device predicate of §2.1 / Alg. 1 (Full iff the score
+// exceeds the threshold or is nonfinite), with on-device compaction of the
+// flagged requests.  No score is read by the host (App. A.5).
+//
+// fp32 weights and arithmetic (App. A.2).  Each dense layer is one launch of a
+// batched GEMV kernel: a wavefront owns one output row for up to 8 requests,
+// streams the row with 16-byte loads, eight 256-float chunks in flight (the
+// weights are read once per batch tile), and reduces across the wavefront.
+// (Dependent launches on one stream start back to back; a grid-wide barrier
+// inside one persistent kernel costs far more on this part.)  RMSNorm of the layer input is
+// folded into the same pass (the sum of squares is accumulated next to the
+// dot products), so the normalised input is never materialised.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <cmath>
+#include <utility>
+
+#include "oda.h"
+#include "oda_internal.h"
+
+namespace {
+
+constexpr int kBatchTile = 8;     // requests per wavefront
+constexpr int kWaves = 4;         // wavefronts per workgroup
+
+enum Mode { kTower = 0, kMlpHidden = 1, kFusion = 2, kGateUp = 3, kDown = 4 };
+
+struct LinArgs {
+  const float* W;        // [rows][K] (kTower: tower 0's weight; the others follow at w_stride)
+  const float* W2;       // kGateUp: the up projection [rows][K]
+  const float* bias;     // [rows] or per tower at w_stride
+  const float* gain;     // RMSNorm gain [K] (kTower: per tower at w_stride; kGateUp)
+  const float* X[3];     // inputs [B][K] (kTower: three; else X[0])
+  const float* aux;      // kFusion: tower outputs [3][B][dt]; kDown: residual [B][rows]
+  float* Y;              // outputs
+  int64_t w_stride;      // kTower: floats between the towers' parameter segments
+  int rows, K, B, dt;
+  float eps;
+};
+
+__device__ __forceinline__ float silu(float x) { return x / (1.f + __expf(-x)); }
+__device__ __forceinline__ float gelu(float x) { return 0.5f * x * (1.f + erff(x * 0.70710678118654752f)); }
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int s = 32; s >= 1; s >>= 1) x += __shfl_xor(x, s);
+  return x;
+}
+__device__ __forceinline__ float dot4(float4 a, float4 b) { return a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w; }
+__device__ __forceinline__ float4 mul4(float4 a, float4 b) { return make_float4(a.x * b.x, a.y * b.y, a.z * b.z, a.w * b.w); }
+__device__ __forceinline__ float4 absdiff4(float4 a, float4 b) {
+  return make_float4(fabsf(a.x - b.x), fabsf(a.y - b.y), fabsf(a.z - b.z), fabsf(a.w - b.w));
+}
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Interaction vector u = [a; b; c; a*b; |a-b|; a*c; |a-c|; b*c; |b-c|]
+// (App. A.2), four consecutive entries starting at k (all in one part).
+__device__ __forceinline__ float4 interaction4(const float* abc, int B, int dt, int b, int k) {
+  const int part = k / dt, m = k - part * dt;
+  const float4 a = *reinterpret_cast<const float4*>(abc + ((int64_t)0 * B + b) * dt + m);
+  const float4 bb = *reinterpret_cast<const float4*>(abc + ((int64_t)1 * B + b) * dt + m);
+  const float4 c = *reinterpret_cast<const float4*>(abc + ((int64_t)2 * B + b) * dt + m);
+  switch (part) {
+    case 0: return a;
+    case 1: return bb;
+    case 2: return c;
+    case 3: return mul4(a, bb);
+    case 4: return absdiff4(a, bb);
+    case 5: return mul4(a, c);
+    case 6: return absdiff4(a, c);
+    case 7: return mul4(bb, c);
+    default: return absdiff4(bb, c);
+  }
+}
+
+template <int MODE>
+__global__ __launch_bounds__(256) void gate_linear_kernel(LinArgs p) {
+  constexpr bool kNorm = (MODE == kTower || MODE == kGateUp);
+  constexpr bool kTwo = (MODE == kGateUp);
+  const int lane = threadIdx.x & 63;
+  const int wave = uniform(threadIdx.x >> 6);
+  const int gw = blockIdx.x * kWaves + wave;
+  const int row0 = gw % p.rows;           // one output row per wavefront
+  const int b0 = (gw / p.rows) * kBatchTile;
+  if (b0 >= p.B) return;
+  const int nb = min(kBatchTile, p.B - b0);
+
+  const float* W = p.W;
+  const float* bias = p.bias;
+  const float* gain = p.gain;
+  const float* X = p.X[0];
+  int tower = 0, row = row0;
+  if (MODE == kTower) {
+    tower = row0 / p.dt;
+    row = row0 - tower * p.dt;
+    W += tower * p.w_stride;
+    bias += tower * p.w_stride;
+    gain += tower * p.w_stride;
+    X = p.X[tower];
+  }
+  const float* wrow = W + (int64_t)row * p.K;
+  const float* wrow2 = kTwo ? p.W2 + (int64_t)row * p.K : nullptr;
+
+  float acc[kBatchTile], acc2[kBatchTile], ss[kBatchTile];
+#pragma unroll
+  for (int bi = 0; bi < kBatchTile; ++bi) acc[bi] = acc2[bi] = ss[bi] = 0.f;
+
+  auto step = [&](int k) {
+    const float4 w = *reinterpret_cast<const float4*>(wrow + k);
+    float4 w2 = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (kTwo) w2 = *reinterpret_cast<const float4*>(wrow2 + k);
+    float4 gk = make_float4(1.f, 1.f, 1.f, 1.f);
+    if (kNorm) gk = *reinterpret_cast<const float4*>(gain + k);
+#pragma unroll
+    for (int bi = 0; bi < kBatchTile; ++bi) {
+      if (bi < nb) {
+        const int b = b0 + bi;
+        float4 x;
+        if (MODE == kFusion) {
+          x = interaction4(p.aux, p.B, p.dt, b, k);
+        } else {
+          x = *reinterpret_cast<const float4*>(X + (int64_t)b * p.K + k);
+        }
+        if (kNorm) ss[bi] += dot4(x, x);
+        const float4 xg = kNorm ? mul4(x, gk) : x;
+        acc[bi] += dot4(w, xg);
+        if (kTwo) acc2[bi] += dot4(w2, xg);
+      }
+    }
+  };
+  // whole 256-float chunks (every lane busy), unrolled so their loads overlap
+  const int full = p.K / 256;
+#pragma unroll 8
+  for (int c = 0; c < full; ++c) step(c * 256 + 4 * lane);
+  if (full * 256 + 4 * lane < p.K) step(full * 256 + 4 * lane);
+
+  // reduce; lane bi finishes request b0 + bi
+  float mine = 0.f, mine2 = 0.f, my_ss = 0.f;
+#pragma unroll
+  for (int bi = 0; bi < kBatchTile; ++bi) {
+    if (bi < nb) {
+      const float s = kNorm ? wave_sum(ss[bi]) : 0.f;
+      const float v = wave_sum(acc[bi]);
+      const float v2 = kTwo ? wave_sum(acc2[bi]) : 0.f;
+      if (lane == bi) {
+        mine = v;
+        mine2 = v2;
+        my_ss = s;
+      }
+    }
+  }
+  if (lane >= nb) return;
+  const int b = b0 + lane;
+  const float inv = kNorm ? rsqrtf(my_ss / (float)p.K + p.eps) : 1.f;
+  if (MODE == kTower) {
+    p.Y[((int64_t)tower * p.B + b) * p.dt + row] = silu(mine * inv + bias[row]);
+  } else if (MODE == kMlpHidden) {
+    p.Y[(int64_t)b * p.rows + row] = gelu(mine + bias[row]);
+  } else if (MODE == kFusion) {
+    const float* abc = p.aux;
+    const float s3 = abc[((int64_t)0 * p.B + b) * p.dt + row] + abc[((int64_t)1 * p.B + b) * p.dt + row] +
+                     abc[((int64_t)2 * p.B + b) * p.dt + row];
+    p.Y[(int64_t)b * p.rows + row] = 0.5f * (s3 + silu(mine + bias[row]));
+  } else if (MODE == kGateUp) {
+    p.Y[(int64_t)b * p.rows + row] = silu(mine * inv) * (mine2 * inv);
+  } else {  // kDown
+    p.Y[(int64_t)b * p.rows + row] = p.aux[(int64_t)b * p.rows + row] + mine;
+  }
+}
+
+struct FinalArgs {
+  const float* X;       // [B][K]: z2 (paper head) or the MLP hidden layer
+  const float* gain;    // paper head: final RMSNorm gain [K]; MLP: NULL
+  const float* w;       // [K]
+  const float* bias;    // [1]
+  const int32_t* forced;
+  float* score;
+  int32_t* flags;
+  int32_t* work_list;
+  int32_t* n_work;
+  int64_t* counter;
+  int K, B;
+  float eps, tau;
+};
+
+// One wavefront: the scalar projection for every request, then the decision
+// and the ascending compaction (ballot + prefix popcount).
+__global__ __launch_bounds__(64) void gate_final_kernel(FinalArgs p) {
+  const int lane = threadIdx.x;
+  const bool norm = p.gain != nullptr;
+  int total = 0;
+  for (int c0 = 0; c0 < p.B; c0 += 64) {
+    float my_score = 0.f;
+    const int nc = min(64, p.B - c0);
+    for (int i = 0; i < nc; ++i) {
+      const int b = c0 + i;
+      float dot = 0.f, ss = 0.f;
+      for (int k = 4 * lane; k < p.K; k += 256) {
+        const float4 x = *reinterpret_cast<const float4*>(p.X + (int64_t)b * p.K + k);
+        float4 wk = *reinterpret_cast<const float4*>(p.w + k);
+        if (norm) {
+          ss += dot4(x, x);
+          wk = mul4(wk, *reinterpret_cast<const float4*>(p.gain + k));
+        }
+        dot += dot4(wk, x);
+      }
+      dot = wave_sum(dot);
+      float s = dot;
+      if (norm) s = dot * rsqrtf(wave_sum(ss) / (float)p.K + p.eps);
+      s += p.bias[0];
+      if (lane == i) my_score = s;
+    }
+    const int b = c0 + lane;
+    bool flag = false;
+    if (lane < nc) {
+      p.score[b] = my_score;
+      flag = p.forced ? (p.forced[b] != 0) : (my_score > p.tau);
+      flag = flag || !__builtin_isfinite(my_score);
+      p.flags[b] = flag ? 1 : 0;
+    }
+    const uint64_t mask = __ballot(flag);
+    if (flag && p.work_list) {
+      const uint64_t below = lane ? (mask & ((~0ull) >> (64 - lane))) : 0ull;
+      p.work_list[total + __popcll(below)] = b;
+    }
+    total += __popcll(mask);
+  }
+  if (lane == 0) {
+    if (p.n_work) p.n_work[0] = total;
+    if (p.counter) p.counter[0] += total;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+
+struct HeadLayout {   // float offsets into the packed parameters (PAPER)
+  int64_t tower_stride, tower_rms, tower_w, tower_b;
+  int64_t wf, bf;
+  int64_t block_stride, blk_rms, blk_gate, blk_up, blk_down;
+  int64_t rms_o, w_o, b_o, total;
+};
+
+HeadLayout paper_layout(int64_t d, int64_t dt) {
+  HeadLayout L;
+  L.tower_stride = d + dt * d + dt;
+  L.tower_rms = 0;
+  L.tower_w = d;
+  L.tower_b = d + dt * d;
+  L.wf = 3 * L.tower_stride;
+  L.bf = L.wf + 9 * dt * dt;
+  const int64_t b0 = L.bf + dt;
+  L.block_stride = dt + 6 * dt * dt;
+  L.blk_rms = b0;
+  L.blk_gate = b0 + dt;
+  L.blk_up = b0 + dt + 2 * dt * dt;
+  L.blk_down = b0 + dt + 4 * dt * dt;
+  L.rms_o = b0 + 2 * L.block_stride;
+  L.w_o = L.rms_o + dt;
+  L.b_o = L.w_o + dt;
+  L.total = L.b_o + 1;
+  return L;
+}
+
+struct GateWs {
+  size_t abc, z0, z1, hdn, hid, bytes;
+};
+
+GateWs gate_ws_layout(int kind, int64_t B, int64_t dt) {
+  GateWs w{};
+  size_t off = 0;
+  auto take = [&](int64_t floats) {
+    const size_t o = off;
+    off += (size_t)oda::round_up(floats * 4, 256);
+    return o;
+  };
+  if (kind == ODA_HEAD_PAPER) {
+    w.abc = take(3 * B * dt);
+    w.z0 = take(B * dt);
+    w.z1 = take(B * dt);
+    w.hdn = take(2 * B * dt);
+  } else {
+    w.hid = take(B * dt);
+  }
+  w.bytes = std::max<size_t>(off, 256);
+  return w;
+}
+
+oda_status check_gate(const oda_gate_desc* g) {
+  if (g == nullptr) return oda::fail(ODA_ERR_NULL, "gate is NULL");
+  if (g->kind != ODA_HEAD_PAPER && g->kind != ODA_HEAD_MLP)
+    return oda::fail(ODA_ERR_UNSUPPORTED, "unknown head kind %d", g->kind);
+  if (g->d_model < 4 || g->d_hidden < 4 || g->d_model % 4 || g->d_hidden % 4)
+    return oda::fail(ODA_ERR_SHAPE, "d_model (%d) and d_hidden (%d) must be positive multiples of 4",
+                     g->d_model, g->d_hidden);
+  if (!(g->rms_eps >= 0.f) || !std::isfinite(g->rms_eps)) return oda::fail(ODA_ERR_SHAPE, "rms_eps must be >= 0");
+  return ODA_OK;
+}
+
+template <int MODE>
+void launch_linear(const LinArgs& a, hipStream_t stream) {
+  const int waves = a.rows * (int)oda::ceil_div(a.B, kBatchTile);
+  hipLaunchKernelGGL(gate_linear_kernel<MODE>, dim3((unsigned)oda::ceil_div(waves, kWaves)), dim3(256), 0,
+                     stream, a);
+}
+
+}  // namespace
+
+extern "C" oda_status oda_gate_param_count(int32_t kind, int32_t d_model, int32_t d_hidden, int64_t* count) {
+  if (count == nullptr) return oda::fail(ODA_ERR_NULL, "count is NULL");
+  if (d_model < 1 || d_hidden < 1) return oda::fail(ODA_ERR_SHAPE, "d_model and d_hidden must be >= 1");
+  if (kind == ODA_HEAD_PAPER) {
+    *count = paper_layout(d_model, d_hidden).total;
+  } else if (kind == ODA_HEAD_MLP) {
+    *count = (int64_t)d_hidden * d_model + 2 * (int64_t)d_hidden + 1;
+  } else {
+    return oda::fail(ODA_ERR_UNSUPPORTED, "unknown head kind %d", kind);
+  }
+  return oda::ok();
+}
+
+extern "C" oda_status oda_gate_workspace_size(const oda_gate_desc* gate, int32_t batch, size_t* bytes) {
+  oda_status st = check_gate(gate);
+  if (st != ODA_OK) return st;
+  if (bytes == nullptr) return oda::fail(ODA_ERR_NULL, "bytes is NULL");
+  if (batch < 1) return oda::fail(ODA_ERR_SHAPE, "batch must be >= 1");
+  *bytes = gate_ws_layout(gate->kind, batch, gate->d_hidden).bytes;
+  return oda::ok();
+}
+
+extern "C" oda_status oda_recall_gate(const oda_gate_desc* gate, int32_t batch, const float* h_prev,
+                                     const float* emb, const float* h_local, float tau, const int32_t* forced,
+                                     float* score, int32_t* flags, int32_t* work_list, int32_t* n_work,
+                                     int64_t* recall_counter, void* workspace, size_t workspace_bytes,
+                                     hipStream_t stream) {
+  oda_status st = check_gate(gate);
+  if (st != ODA_OK) return st;
+  if (batch < 1) return oda::fail(ODA_ERR_SHAPE, "batch must be >= 1");
+  const bool paper = gate->kind == ODA_HEAD_PAPER;
+  if (!gate->params || !h_local || !score || !flags || (paper && (!h_prev || !emb)))
+    return oda::fail(ODA_ERR_NULL, "params, h_local, score, flags (and h_prev, emb for the paper head) are required");
+  if ((work_list == nullptr) != (n_work == nullptr))
+    return oda::fail(ODA_ERR_NULL, "work_list and n_work must both be NULL or both be set");
+  if (std::isnan(tau)) return oda::fail(ODA_ERR_SHAPE, "tau is NaN");
+  if (!oda::aligned(gate->params, 16) || !oda::aligned(h_local, 16) ||
+      (paper && (!oda::aligned(h_prev, 16) || !oda::aligned(emb, 16))))
+    return oda::fail(ODA_ERR_SHAPE, "params and gate inputs must be 16-byte aligned");
+  const GateWs ws = gate_ws_layout(gate->kind, batch, gate->d_hidden);
+  if (workspace == nullptr) return oda::fail(ODA_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", ws.bytes);
+  if (workspace_bytes < ws.bytes)
+    return oda::fail(ODA_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", workspace_bytes, ws.bytes);
+  if (!oda::aligned(workspace, 256)) return oda::fail(ODA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+
+  char* wsb = static_cast<char*>(workspace);
+  const int d = gate->d_model, dt = gate->d_hidden;
+  const float* P = gate->params;
+  (void)hipGetLastError();
+  FinalArgs fa{};
+  fa.B = batch;
+  fa.eps = gate->rms_eps;
+  fa.tau = tau;
+  fa.forced = forced;
+  fa.score = score;
+  fa.flags = flags;
+  fa.work_list = work_list;
+  fa.n_work = n_work;
+  fa.counter = recall_counter;
+  if (paper) {
+    const HeadLayout H = paper_layout(d, dt);
+    float* abc = reinterpret_cast<float*>(wsb + ws.abc);
+    float* z0 = reinterpret_cast<float*>(wsb + ws.z0);
+    float* z1 = reinterpret_cast<float*>(wsb + ws.z1);
+    float* hdn = reinterpret_cast<float*>(wsb + ws.hdn);
+    LinArgs a{};
+    a.B = batch;
+    a.dt = dt;
+    a.eps = gate->rms_eps;
+    // towers: a, b, c = SiLU(W_t RMSNorm(x_t) + b_t)
+    a.W = P + H.tower_w;
+    a.bias = P + H.tower_b;
+    a.gain = P + H.tower_rms;
+    a.w_stride = H.tower_stride;
+    a.X[0] = h_prev;
+    a.X[1] = emb;
+    a.X[2] = h_local;
+    a.Y = abc;
+    a.rows = 3 * dt;
+    a.K = d;
+    launch_linear<kTower>(a, stream);
+    // fusion: z0 = (a + b + c + SiLU(W_f u + b_f)) / 2
+    a = LinArgs{};
+    a.B = batch;
+    a.dt = dt;
+    a.eps = gate->rms_eps;
+    a.W = P + H.wf;
+    a.bias = P + H.bf;
+    a.aux = abc;
+    a.Y = z0;
+    a.rows = dt;
+    a.K = 9 * dt;
+    launch_linear<kFusion>(a, stream);
+    // two pre-RMSNorm residual SwiGLU blocks
+    float* zin = z0;
+    float* zout = z1;
+    for (int k = 0; k < 2; ++k) {
+      const int64_t base = k * H.block_stride;
+      a = LinArgs{};
+      a.B = batch;
+      a.dt = dt;
+      a.eps = gate->rms_eps;
+      a.W = P + H.blk_gate + base;
+      a.W2 = P + H.blk_up + base;
+      a.gain = P + H.blk_rms + base;
+      a.X[0] = zin;
+      a.Y = hdn;
+      a.rows = 2 * dt;
+      a.K = dt;
+      launch_linear<kGateUp>(a, stream);
+      a = LinArgs{};
+      a.B = batch;
+      a.dt = dt;
+      a.W = P + H.blk_down + base;
+      a.X[0] = hdn;
+      a.aux = zin;
+      a.Y = zout;
+      a.rows = dt;
+      a.K = 2 * dt;
+      launch_linear<kDown>(a, stream);
+      std::swap(zin, zout);
+    }
+    // q = w_o . RMSNorm(z2) + b_o
+    fa.X = zin;
+    fa.gain = P + H.rms_o;
+    fa.w = P + H.w_o;
+    fa.bias = P + H.b_o;
+    fa.K = dt;
+  } else {
+    float* hid = reinterpret_cast<float*>(wsb + ws.hid);
+    LinArgs a{};
+    a.B = batch;
+    a.dt = dt;
+    a.W = P;
+    a.bias = P + (int64_t)dt * d;
+    a.X[0] = h_local;
+    a.Y = hid;
+    a.rows = dt;
+    a.K = d;
+    launch_linear<kMlpHidden>(a, stream);
+    fa.X = hid;
+    fa.gain = nullptr;
+    fa.w = P + (int64_t)dt * d + dt;
+    fa.bias = P + (int64_t)dt * d + 2 * dt;
+    fa.K = dt;
+  }
+  hipLaunchKernelGGL(gate_final_kernel, dim3(1), dim3(64), 0, stream, fa);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return oda::fail(ODA_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return oda::ok();
+}

@@ -1,0 +1,135 @@
+"""The C-ABI library loads, exports every entry point include/oda.h declares,
+and rejects bad arguments with the documented status codes before touching the
+GPU (no device work is needed, so these run without one)."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2609_20734_amd import build as B
+    if not os.path.exists(B.LIB):
+        B.build()
+    import paper_2609_20734_amd._lib as lib
+    return lib
+
+
+def declared_functions():
+    txt = open(os.path.join(ROOT, "include", "oda.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(oda_[a-z_0-9]+)\s*\(", txt)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert set(names) == set(L.EXPORTED), names
+    for n in names:
+        assert hasattr(L._lib, n), n
+
+
+def _shape(L, **kw):
+    base = dict(num_layers=2, batch=3, num_q_heads=8, num_kv_heads=2, head_dim=128, max_blocks_per_seq=4,
+                max_seq_len=64, num_blocks=20, split_blocks=0)
+    base.update(kw)
+    return L.Shape(**base)
+
+
+def test_param_count_matches_paper(L):
+    assert L.gate_param_count(L.HEAD_PAPER, 2048, 1024) == 28_325_889       # App. A.2
+    assert L.gate_param_count(L.HEAD_MLP, 4096, 256) == 4096 * 256 + 2 * 256 + 1
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(num_layers=0), -2), (dict(batch=0), -2), (dict(num_q_heads=7), -2), (dict(head_dim=96), -3),
+    (dict(num_q_heads=2 * 17, num_kv_heads=2), -3), (dict(block_size=32), -3), (dict(max_seq_len=0), -2),
+    (dict(max_blocks_per_seq=3), -2), (dict(num_blocks=0), -2), (dict(split_blocks=3), -2),
+    (dict(split_blocks=2048), -2)])
+def test_bad_shapes(L, kw, status):
+    with pytest.raises(L.OdaError) as e:
+        L.attn_workspace_size(_shape(L, **kw), 4, 16)
+    assert e.value.status == status
+    assert L.last_error()
+
+
+def test_workspace_size_scales_with_window(L):
+    s = _shape(L, max_seq_len=64 * 1024, max_blocks_per_seq=4096)
+    small = L.attn_workspace_size(s, 4, 1024)
+    full = L.attn_workspace_size(s, 0, 0)
+    assert 0 < small <= full and small % 256 == 0 and full % 256 == 0
+
+
+def _inputs(L, **kw):
+    base = dict(q=0x1000, k_cache=0x2000, v_cache=0x3000, block_table=0x4000, seq_lens=0x5000, scale=0.125)
+    base.update(kw)
+    return L.inputs(base["q"], base["k_cache"], base["v_cache"], base["block_table"], base["seq_lens"],
+                    base["scale"], base.get("k_cur"), base.get("v_cur"))
+
+
+def test_local_rejects_bad_arguments_without_launching(L):
+    s = _shape(L)
+    ws_bytes = L.attn_workspace_size(s, 4, 16)
+    cases = [
+        (dict(q=None), 0x9000, 0x100000, ws_bytes, 4, 16, -1),
+        (dict(k_cur=0x6000), 0x9000, 0x100000, ws_bytes, 4, 16, -1),            # v_cur missing
+        (dict(q=0x1008), 0x9000, 0x100000, ws_bytes, 4, 16, -2),                # misaligned
+        (dict(scale=0.0), 0x9000, 0x100000, ws_bytes, 4, 16, -2),
+        (dict(scale=math.inf), 0x9000, 0x100000, ws_bytes, 4, 16, -2),
+        (dict(), None, 0x100000, ws_bytes, 4, 16, -1),                          # out NULL
+        (dict(), 0x9000, None, ws_bytes, 4, 16, -4),                            # no workspace
+        (dict(), 0x9000, 0x100000, ws_bytes - 1, 4, 16, -4),                    # too small
+        (dict(), 0x9000, 0x100010, ws_bytes, 4, 16, -4),                        # misaligned workspace
+        (dict(), 0x9000, 0x100000, ws_bytes, -1, 16, -2),
+        (dict(), 0x9000, 0x100000, ws_bytes, 4, 0, -2),                         # Local needs a window
+    ]
+    for kw, out, ws, wb, s_, w_, status in cases:
+        with pytest.raises(L.OdaError) as e:
+            L.local_decode_attn(s, _inputs(L, **kw), s_, w_, out, None, ws, workspace_bytes=wb, stream=0)
+        assert e.value.status == status, (kw, e.value)
+
+
+def test_full_rejects_bad_arguments(L):
+    s = _shape(L)
+    wb = L.attn_workspace_size(s, 0, 0)
+    with pytest.raises(L.OdaError) as e:
+        L.full_decode_attn(s, _inputs(L), 0, None, 0x7000, None, 0x9000, None, 0x100000, wb, stream=0)
+    assert e.value.status == -1                                            # work_list without n_work
+    with pytest.raises(L.OdaError) as e:
+        L.full_decode_attn(s, _inputs(L), -5, None, None, None, 0x9000, None, 0x100000, wb, stream=0)
+    assert e.value.status == -2
+
+
+def test_gate_rejects_bad_arguments(L):
+    g = L.gate_desc(L.HEAD_PAPER, 64, 16, 0x8000)
+    wb = L.gate_workspace_size(g, 4)
+    ok = dict(h_prev=0x1000, emb=0x2000, h_local=0x3000, score=0x4000, flags=0x5000)
+
+    def call(gate=g, batch=4, tau=0.0, ws=0x100000, wbytes=wb, **kw):
+        a = dict(ok)
+        a.update(kw)
+        L.recall_gate(gate, batch, a["h_prev"], a["emb"], a["h_local"], tau, None, a["score"], a["flags"],
+                      a.get("work_list"), a.get("n_work"), None, ws, wbytes, stream=0)
+
+    for kw, status in [(dict(emb=None), -1), (dict(score=None), -1), (dict(batch=0), -2), (dict(tau=math.nan), -2),
+                       (dict(ws=None), -4), (dict(wbytes=wb - 1), -4), (dict(work_list=0x6000), -1),
+                       (dict(gate=L.gate_desc(7, 64, 16, 0x8000)), -3), (dict(gate=L.gate_desc(0, 62, 16, 0x8000)), -2),
+                       (dict(gate=L.gate_desc(0, 64, 16, 0x8004)), -2)]:
+        with pytest.raises(L.OdaError) as e:
+            call(**kw)
+        assert e.value.status == status, (kw, e.value)
+    # the MLP stand-in needs only h_local
+    gm = L.gate_desc(L.HEAD_MLP, 64, 16, 0x8000)
+    with pytest.raises(L.OdaError) as e:
+        L.recall_gate(gm, 4, None, None, None, 0.0, None, 0x4000, 0x5000, None, None, None, 0x100000,
+                      L.gate_workspace_size(gm, 4), stream=0)
+    assert e.value.status == -1
+
+
+def test_status_strings(L):
+    for s in (0, -1, -2, -3, -4, -5):
+        assert L.status_string(s).startswith("ODA_")

@@ -1,0 +1,157 @@
+"""GPU parity of oda_local_decode_attn / oda_full_decode_attn against the
+fp64 oracle, element by element."""
+import numpy as np
+import pytest
+import torch
+
+import oda_synth as S
+from harness import LSE_ABS, AttnProblem, check_close, dev_i32
+from oracle import attention as OA
+
+pytestmark = pytest.mark.gpu
+
+
+def _cmp(prob, got, ref, requests=None):
+    out, lse = got
+    o_ref, l_ref, _ = ref
+    o = out.cpu().numpy()
+    l = lse.cpu().numpy()
+    reqs = range(prob.B) if requests is None else requests
+    for b in reqs:
+        check_close(o[:, b], o_ref[:, b], what=f"out[:, {b}]")
+        assert np.max(np.abs(l[:, b] - l_ref[:, b])) <= LSE_ABS
+
+
+def test_tiny_config_local_and_full():
+    """Tiny: 1 layer, 8q/2kv heads, D=64, n=1024, W=128, contiguous KV."""
+    p = AttnProblem(1234, 1, 1, 8, 2, 64, [1024], permute=False)
+    _cmp(p, p.run_local(4, 128), p.oracle_local(4, 128))
+    _cmp(p, p.run_full(0), p.oracle_full(0))
+
+
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("G", [1, 2, 4, 8, 16])
+def test_shapes_and_gqa_groups(D, G):
+    Hkv = 2
+    p = AttnProblem(10 + G + D, 2, 3, Hkv * G, Hkv, D, [1, 45, 333], permute=True, split_blocks=4)
+    _cmp(p, p.run_local(4, 37), p.oracle_local(4, 37))
+    _cmp(p, p.run_full(0), p.oracle_full(0))
+
+
+@pytest.mark.parametrize("cur", [False, True])
+@pytest.mark.parametrize("split_blocks", [2, 6, 0])
+def test_boundary_lengths(cur, split_blocks):
+    """n at every boundary of the access set: 1, s, s+1, W-1, W, W+1, s+W, s+W+1,
+    partial first/last blocks, with the current token from the cache or k_cur."""
+    s, W = 4, 40
+    seq = [1, s, s + 1, W - 1, W, W + 1, s + W, s + W + 1, 16, 17, 63, 64, 65, 200]
+    p = AttnProblem(77, 2, len(seq), 8, 2, 128, seq, cur=cur, split_blocks=split_blocks)
+    _cmp(p, p.run_local(s, W), p.oracle_local(s, W))
+    _cmp(p, p.run_local(0, W), p.oracle_local(0, W))
+    _cmp(p, p.run_full(0), p.oracle_full(0))
+    _cmp(p, p.run_full(W), p.oracle_full(W))
+
+
+@pytest.mark.parametrize("s", [0, 1, 4, 16, 19, 33])
+def test_sink_counts_and_shared_block(s):
+    """Sinks spanning one or several blocks, and a block shared by the sink and
+    the recent part."""
+    seq = [20, 40, 50, 70, 100, 300]
+    p = AttnProblem(5 + s, 1, len(seq), 4, 1, 64, seq, split_blocks=2)
+    for W in (1, 8, 30, 64):
+        _cmp(p, p.run_local(s, W), p.oracle_local(s, W))
+
+
+def test_local_equals_full_when_window_covers_context():
+    """P1 on the GPU: s + W >= n gives the same set; the two calls agree within
+    fp32 rounding (different split plans) and both match the oracle."""
+    seq = [1, 30, 200, 257]
+    p = AttnProblem(3, 2, len(seq), 16, 4, 128, seq)
+    loc = p.run_local(4, 260)
+    full = p.run_full(0)
+    np.testing.assert_allclose(loc[0].cpu().numpy(), full[0].cpu().numpy(), atol=2e-6, rtol=0)
+    _cmp(p, loc, p.oracle_full(0))
+
+
+@pytest.mark.parametrize("mode", ["flags", "list"])
+def test_full_touches_only_selected_requests(mode):
+    seq = [100, 37, 260, 5, 99]
+    p = AttnProblem(9, 2, len(seq), 8, 2, 64, seq, split_blocks=2)
+    sel = np.array([0, 1, 1, 0, 1], dtype=np.int32)
+    out, lse = p.new_out(-7.0)
+    if mode == "flags":
+        p.run_full(0, flags=dev_i32(sel), out=out, lse=lse)
+    else:
+        wl = np.zeros(len(seq), np.int32)
+        idx = np.flatnonzero(sel)
+        wl[:len(idx)] = idx
+        wl[len(idx):] = 0   # entries past n_work are never read as requests
+        p.run_full(0, work_list=dev_i32(wl), n_work=dev_i32([len(idx)]), out=out, lse=lse)
+    o = out.cpu().numpy()
+    ref = p.oracle_full(0, requests=list(np.flatnonzero(sel)))
+    for b in range(len(seq)):
+        if sel[b]:
+            check_close(o[:, b], ref[0][:, b])
+        else:
+            assert np.all(o[:, b] == -7.0) and np.all(lse.cpu().numpy()[:, b] == -7.0)
+
+
+def test_empty_work_list_writes_nothing():
+    p = AttnProblem(2, 1, 3, 8, 2, 64, [10, 20, 30])
+    out, lse = p.new_out(3.5)
+    p.run_full(0, work_list=dev_i32([0, 0, 0]), n_work=dev_i32([0]), out=out, lse=lse)
+    assert torch.all(out == 3.5) and torch.all(lse == 3.5)
+
+
+def test_reruns_are_bit_identical():
+    seq = [333, 1000]
+    p = AttnProblem(4, 2, 2, 32, 8, 128, seq)
+    a = p.run_local(4, 256)
+    b = p.run_local(4, 256)
+    c = p.run_full(0)
+    d = p.run_full(0)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+    assert torch.equal(c[0], d[0]) and torch.equal(c[1], d[1])
+
+
+@pytest.mark.parametrize("n,s,W", [(300, 4, 64), (300, 0, 64), (70, 4, 66), (129, 19, 50)])
+def test_dominant_key_probes(n, s, W):
+    """P10 on the GPU: a key aligned with q at position p dominates iff p is in
+    the access set, so out ~ V_p exactly at the set's boundaries."""
+    p = AttnProblem(8, 1, 1, 1, 1, 64, [n], split_blocks=2)
+    p.q[:] = S.f32_to_bf16_bits(np.float32(1.0))
+    p.k = S.f32_to_bf16_bits(S.bf16_bits_to_f32(p.k) * np.float32(0.05))
+    members = set(OA.local_set(n, s, W).tolist())
+    for pos in sorted({0, s - 1, s, n - W - 1, n - W, n - 1}):
+        if not (0 <= pos < n):
+            continue
+        k = p.k.copy()
+        k[0, p.table[0][pos // 16], 0, :, pos % 16, :] = S.f32_to_bf16_bits(np.float32(8.0))
+        saved = p.k
+        p.k = k
+        p.upload()
+        out, _ = p.run_local(s, W)
+        ref = p.oracle_local(s, W)
+        check_close(out.cpu().numpy(), ref[0])
+        vp = OA.bf16_to_f64(p.v[0, p.table[0][pos // 16], 0, :, pos % 16])
+        hit = np.max(np.abs(out.cpu().numpy()[0, 0, 0] - vp)) < 1e-5
+        assert hit == (pos in members), (pos, hit)
+        p.k = saved
+    p.upload()
+
+
+def test_nan_in_unattended_slots_is_ignored():
+    """Slots outside the access set may hold anything; NaN there must not leak."""
+    seq = [40, 23]
+    p = AttnProblem(6, 1, 2, 8, 2, 128, seq, split_blocks=2)
+    nanbits = np.uint16(0x7FC0)
+    for b, n in enumerate(seq):
+        for pos in range(n, ((n + 15) // 16) * 16):       # tail of the last block
+            p.k[:, p.table[b][pos // 16], :, :, pos % 16, :] = nanbits
+            p.v[:, p.table[b][pos // 16], :, :, pos % 16] = nanbits
+        for pos in range(4, 16):                          # between sinks and window
+            if pos < n - 8:
+                p.k[:, p.table[b][0], :, :, pos, :] = nanbits
+                p.v[:, p.table[b][0], :, :, pos] = nanbits
+    p.upload()
+    _cmp(p, p.run_local(4, 8), p.oracle_local(4, 8))
