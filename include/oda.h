@@ -82,8 +82,8 @@ typedef struct {
   int32_t max_blocks_per_seq; /* row stride of block_table (>= ceil(max_seq_len/16)) */
   int32_t max_seq_len;        /* host-known upper bound of seq_lens[]             */
   int64_t num_blocks;         /* physical blocks per layer in k_cache / v_cache   */
-  int32_t split_blocks;       /* KV blocks per split-K work item: 0 = automatic,
-                                 otherwise an even number in [2, 1024]            */
+  int32_t split_blocks;       /* KV blocks per split-K work item (one workgroup
+                                 each): 0 = automatic, otherwise an even number >= 2 */
   int32_t reserved;           /* must be 0                                        */
 } oda_attn_shape;
 
@@ -103,9 +103,11 @@ typedef struct {
   float scale;                  /* softmax scale (> 0), usually 1/sqrt(D)         */
 } oda_attn_inputs;
 
-/* Bytes of workspace an attention call with this shape and access set needs.
- * window == 0 means "no window" (the whole history); window > 0 limits the
- * recent part to `window` positions.  n_sink >= 0.  (host out) */
+/* Bytes of workspace an attention call with this shape and access set needs
+ * (split-K partials).  It is 0 when every request fits one work item; the
+ * workspace pointer may then be NULL.  window == 0 means "no window" (the whole
+ * history); window > 0 limits the recent part to `window` positions.
+ * n_sink >= 0.  (host out) */
 oda_status oda_attn_workspace_size(const oda_attn_shape *shape, int32_t n_sink, int32_t window,
                                    size_t *bytes);
 

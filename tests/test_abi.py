@@ -49,7 +49,7 @@ def test_param_count_matches_paper(L):
     (dict(num_layers=0), -2), (dict(batch=0), -2), (dict(num_q_heads=7), -2), (dict(head_dim=96), -3),
     (dict(num_q_heads=2 * 17, num_kv_heads=2), -3), (dict(block_size=32), -3), (dict(max_seq_len=0), -2),
     (dict(max_blocks_per_seq=3), -2), (dict(num_blocks=0), -2), (dict(split_blocks=3), -2),
-    (dict(split_blocks=2048), -2)])
+    (dict(split_blocks=-2), -2)])
 def test_bad_shapes(L, kw, status):
     with pytest.raises(L.OdaError) as e:
         L.attn_workspace_size(_shape(L, **kw), 4, 16)
@@ -58,10 +58,14 @@ def test_bad_shapes(L, kw, status):
 
 
 def test_workspace_size_scales_with_window(L):
-    s = _shape(L, max_seq_len=64 * 1024, max_blocks_per_seq=4096)
+    s = _shape(L, max_seq_len=64 * 1024, max_blocks_per_seq=4096, split_blocks=16)
     small = L.attn_workspace_size(s, 4, 1024)
     full = L.attn_workspace_size(s, 0, 0)
     assert 0 < small <= full and small % 256 == 0 and full % 256 == 0
+    # the automatic plan needs no workspace when one workgroup per (layer, request, head) fills the GPU
+    big = _shape(L, num_layers=32, batch=1, num_q_heads=32, num_kv_heads=8, max_seq_len=32768,
+                 max_blocks_per_seq=2048)
+    assert L.attn_workspace_size(big, 0, 0) == 0
 
 
 def _inputs(L, **kw):
@@ -72,8 +76,9 @@ def _inputs(L, **kw):
 
 
 def test_local_rejects_bad_arguments_without_launching(L):
-    s = _shape(L)
+    s = _shape(L, split_blocks=2)           # several splits per request: a workspace is required
     ws_bytes = L.attn_workspace_size(s, 4, 16)
+    assert ws_bytes > 0
     cases = [
         (dict(q=None), 0x9000, 0x100000, ws_bytes, 4, 16, -1),
         (dict(k_cur=0x6000), 0x9000, 0x100000, ws_bytes, 4, 16, -1),            # v_cur missing
@@ -94,7 +99,7 @@ def test_local_rejects_bad_arguments_without_launching(L):
 
 
 def test_full_rejects_bad_arguments(L):
-    s = _shape(L)
+    s = _shape(L, split_blocks=2)
     wb = L.attn_workspace_size(s, 0, 0)
     with pytest.raises(L.OdaError) as e:
         L.full_decode_attn(s, _inputs(L), 0, None, 0x7000, None, 0x9000, None, 0x100000, wb, stream=0)
