@@ -34,6 +34,35 @@ sys.path.insert(0, ROOT)
 METRIC = "decode-attn µs/step + achieved HBM GB/s vs always-Full, recall rate 0-100%"
 HBM_PEAK_GBS = 8000.0
 HEADLINE_RHO = 0.1
+ROOFLINE_REPS = 20
+ROOFLINE_KERNEL = "attn_split_kernel<128, false>"
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_20734_amd", "csrc", "attention.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "full_split_llama3-8b_traffic.txt")
+
+
+def source_sha256() -> str:
+    import hashlib
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per launch of the roofline kernel from the committed PMC summary,
+    or None if there is none or the kernel source changed since it was taken."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    with open(TRAFFIC_FILE) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("source_sha256") != source_sha256():
+        return None
+    try:
+        return float(vals["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def log(*a):
@@ -285,6 +314,8 @@ def main():
     ap.add_argument("--split-blocks", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--warm", action="store_true", help="also time back-to-back (warm) steps")
+    ap.add_argument("--roofline-only", action="store_true",
+                    help="only the roofline leg (always-Full calls) plus a 1 GiB copy, for PMC profiling")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
@@ -298,11 +329,23 @@ def main():
     K = args.steps
     b = Bench(wl, args.head, args.seed, K, args.split_blocks)
     P = b.P
+    local_b, gate_b, full_b = bytes_for(wl, b.seq_host, None, args.head)
+    bytes_full = sum(full_b)
+
+    if args.roofline_only:
+        t = b.kernel_time(b.full_calls()[0], reps=ROOFLINE_REPS, cold=True)
+        src = torch.ones(1 << 28, dtype=torch.float32, device=b.dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)          # calibration: 1 GiB read + 1 GiB written
+        torch.cuda.synchronize()
+        print(json.dumps({"roofline_only": True, "kernel": ROOFLINE_KERNEL, "us_per_launch": t,
+                          "bytes_per_launch": bytes_full, "reps": ROOFLINE_REPS,
+                          "copy_bytes": 1 << 30, "source_sha256": source_sha256()}), flush=True)
+        return
 
     # always-Full baseline
     full = b.timed(b.full_calls(), args.warmup, cold=True)
-    local_b, gate_b, full_b = bytes_for(wl, b.seq_host, None, args.head)
-    bytes_full = sum(full_b)
     log(f"[bench] always-Full {full['us_mean']:.1f} us/step ({bytes_full / full['us_mean'] / 1e3:.0f} GB/s)")
 
     # rho sweep
@@ -342,13 +385,15 @@ def main():
             log(f"[bench] p={p:.2f} (real {real:.3f}) {r['us_mean']:.1f} us/step ratio {ent['ratio']:.3f} "
                 f"ideal {ent['ideal_ratio']:.3f} x{ent['linearity']:.2f}")
 
-    # roofline of the dominant kernel: the Full split-K pass over all requests
+    # roofline of the dominant kernel: the Full split-K pass over every request
+    # (one launch of attn_split_kernel<128, false>; no merge launch at this size),
+    # the last ROOFLINE_REPS dispatches of that kernel in this process
     fcalls = b.full_calls()[0]
-    t_full_call = b.kernel_time(fcalls, reps=max(5, min(50, K // 4)), cold=True)
+    t_full_call = b.kernel_time(fcalls, reps=ROOFLINE_REPS, cold=True)
     roof = dict(bound="hbm", achieved=bytes_full / t_full_call / 1e3, peak=HBM_PEAK_GBS, unit="GB/s",
-                traffic=None)
+                traffic=measured_traffic())
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["kernel"] = "oda_full_decode_attn (attn_split_kernel<128> + attn_merge_kernel<128>), all requests"
+    roof["kernel"] = ROOFLINE_KERNEL + " (oda_full_decode_attn, every request)"
     roof["bytes_per_launch"] = bytes_full
     roof["us_per_launch"] = t_full_call
 

@@ -85,7 +85,9 @@ struct AttnArgs {
   int32_t L, B, Hq, Hkv, G, MB;
   int32_t n_sink, window;   // window <= 0: no window
   int32_t has_cur;
-  int32_t bps, max_splits;
+  int32_t bps, max_splits;  // bps: blocks per split when fixed by the caller
+  int32_t dyn_splits;       // 1: blocks per split chosen on the device (effective_bps)
+  int32_t nvb_max;          // host bound on visited blocks per request
   int32_t select;
   float scale_log2;         // scale * log2(e)
 };
@@ -147,6 +149,29 @@ __device__ __forceinline__ bool resolve_request(const AttnArgs& a, int slot, int
 }
 
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Blocks per split for this call.  With the automatic plan the split count
+// depends on how many requests are selected (known only on the device for
+// Full): enough splits that the selected requests give about
+// ODA_TARGET_GROUPS workgroups, at most max_splits (sized for one request).
+__device__ __forceinline__ int effective_bps(const AttnArgs& a) {
+  if (!a.dyn_splits) return a.bps;
+  int active = a.B;
+  if (a.select == kSelList) {
+    active = a.n_work[0];
+  } else if (a.select == kSelFlags) {
+    active = 0;
+    for (int b0 = 0; b0 < a.B; b0 += 64) {
+      const int b = b0 + (int)(threadIdx.x & 63);
+      active += __popcll(__ballot(b < a.B && a.flags[b] != 0));
+    }
+  }
+  const int64_t units = (int64_t)max(active, 1) * a.L * a.Hkv;
+  const int64_t want = (ODA_TARGET_GROUPS + units - 1) / units;
+  const int s = (int)max((int64_t)1, min((int64_t)a.max_splits, want));
+  const int bps = ((a.nvb_max + s - 1) / s + 1) & ~1;
+  return uniform(max(bps, 2));
+}
 
 __device__ __forceinline__ bf16x8 load16(const uint16_t* p) {
   return *reinterpret_cast<const bf16x8*>(p);
@@ -331,7 +356,9 @@ __host__ __device__ constexpr size_t split_lds_floats(int G, int D) {
   return (size_t)kWaves * 32 + (size_t)kWaves * G * D + 16;
 }
 
-template <int D>
+// kLocal selects the Local access set (sinks + window); Full instances take the
+// native set (whole history, or a native window) and never have sinks.
+template <int D, bool kLocal>
 __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_split_kernel(AttnArgs a) {
   constexpr int KK = D / 32;   // MFMA k-steps for q.k
@@ -342,28 +369,33 @@ void attn_split_kernel(AttnArgs a) {
   const int h16 = lane & 15;
   const int j = lane >> 4;
 
+  // split outermost, then request slot: the items that have work (the splits in
+  // use, the selected requests of a work list) form a prefix of the grid, so
+  // the dispatcher places them first instead of interleaving them with
+  // workgroups that exit at once
   int64_t item = blockIdx.x;
-  const int split = (int)(item % a.max_splits);
-  item /= a.max_splits;
   const int g = (int)(item % a.Hkv);
   item /= a.Hkv;
+  const int l = (int)(item % a.L);
+  item /= a.L;
   const int slot = (int)(item % a.B);
-  const int l = (int)(item / a.B);
-  if (l >= a.L) return;
+  const int split = (int)(item / a.B);
+  if (split >= a.max_splits) return;
   int b;
   if (!resolve_request(a, slot, b)) return;
   b = uniform(b);
   const int n = uniform(a.seq_lens[b]);
   Run r;
-  r.geo = geometry(n, a.n_sink, a.window, a.has_cur);
+  r.geo = geometry(n, kLocal ? a.n_sink : 0, a.window, a.has_cur);
+  const int bps = effective_bps(a);
   // (nvb = 0 happens only with the candidate as the sole position: one item, no blocks)
-  const int nsplit = max(1, (r.geo.nvb + a.bps - 1) / a.bps);
+  const int nsplit = max(1, (r.geo.nvb + bps - 1) / bps);
   if (split >= nsplit) return;   // uniform over the workgroup: no barrier is skipped by part of it
   const int G = a.G;
 
   // this wavefront's run: a contiguous share of the split's pairs
-  const int v_begin = split * a.bps;
-  const int v_end = min(r.geo.nvb, v_begin + a.bps);
+  const int v_begin = split * bps;
+  const int v_end = min(r.geo.nvb, v_begin + bps);
   const int pairs = (v_end - v_begin + 1) >> 1;
   const int per_wave = (pairs + kWaves - 1) / kWaves;
   r.v_lo = min(v_end, v_begin + 2 * per_wave * wave);
@@ -509,15 +541,16 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(AttnArgs a) {
   int64_t unit = blockIdx.x;
   const int g = (int)(unit % a.Hkv);
   unit /= a.Hkv;
-  const int slot = (int)(unit % a.B);
-  const int l = (int)(unit / a.B);
-  if (l >= a.L) return;
+  const int l = (int)(unit % a.L);
+  const int slot = (int)(unit / a.L);
+  if (slot >= a.B) return;
   int b;
   if (!resolve_request(a, slot, b)) return;
   b = uniform(b);
   const int n = uniform(a.seq_lens[b]);
   const Geometry geo = geometry(n, a.n_sink, a.window, a.has_cur);
-  const int nsplit = max(1, (geo.nvb + a.bps - 1) / a.bps);
+  const int bps = effective_bps(a);
+  const int nsplit = max(1, (geo.nvb + bps - 1) / bps);
   if (nsplit <= 1) return;   // finalized by the split kernel
   const int G = a.G;
   const int lane = threadIdx.x & 63;
@@ -573,6 +606,7 @@ struct Plan {
   int nvb_max;
   int bps;
   int max_splits;
+  int dyn;
   size_t off_ml;
   size_t bytes;
 };
@@ -600,10 +634,12 @@ oda_status check_shape(const oda_attn_shape* s) {
   return ODA_OK;
 }
 
-// Work decomposition.  One workgroup per (layer, request, KV head, split);
-// the automatic plan splits only as much as needed to give the GPU about
-// ODA_TARGET_GROUPS workgroups (one per CU), so most calls finish in the split
-// kernel and skip the merge.
+// Work decomposition.  One workgroup per (request, layer, KV head, split).
+// The automatic plan splits a request only as much as needed for the selected
+// requests to give the GPU about ODA_TARGET_GROUPS workgroups (one per CU):
+// the grid and the workspace are sized for the case of a single selected
+// request (max_splits); the kernels pick the actual split count on the device
+// (effective_bps), so most calls finish in the split kernel.
 void make_plan(const oda_attn_shape* s, int n_sink, int window, Plan* p) {
   const int64_t total_blocks = oda::ceil_div(s->max_seq_len, kBlock);
   int64_t nvb = total_blocks;
@@ -612,13 +648,16 @@ void make_plan(const oda_attn_shape* s, int n_sink, int window, Plan* p) {
     nvb = std::min<int64_t>(total_blocks, sink_blocks + oda::ceil_div(window, kBlock) + 1);
   }
   const int64_t units = (int64_t)s->num_layers * s->batch * s->num_kv_heads;
+  const int64_t units_per_request = (int64_t)s->num_layers * s->num_kv_heads;
   int64_t bps = s->split_blocks;
+  p->dyn = 0;
   if (bps == 0) {
-    const int64_t want = oda::ceil_div(ODA_TARGET_GROUPS, units);
+    const int64_t want = oda::ceil_div(ODA_TARGET_GROUPS, units_per_request);
     // at least 4 blocks per wavefront
     const int64_t max_split = std::max<int64_t>(1, nvb / (4 * kWaves));
     const int64_t nsplit = std::max<int64_t>(1, std::min(want, max_split));
     bps = oda::round_up(oda::ceil_div(nvb, nsplit), 2);
+    p->dyn = 1;
   }
   p->nvb_max = (int)nvb;
   p->bps = (int)std::min<int64_t>(bps, 1 << 30);
@@ -650,7 +689,7 @@ oda_status check_inputs(const oda_attn_inputs* in, const float* out) {
   return ODA_OK;
 }
 
-template <int D>
+template <int D, bool kLocal>
 oda_status launch(const AttnArgs& args, const Plan& plan, hipStream_t stream) {
   const int64_t units = (int64_t)args.L * args.B * args.Hkv;
   const int64_t items = units * plan.max_splits;
@@ -658,12 +697,12 @@ oda_status launch(const AttnArgs& args, const Plan& plan, hipStream_t stream) {
   const size_t lds = split_lds_floats(args.G, D) * sizeof(float);
   static bool lds_raised = false;
   if (!lds_raised) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(attn_split_kernel<D>),
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(attn_split_kernel<D, kLocal>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)(split_lds_floats(kMaxGroup, D) * 4));
     lds_raised = true;
   }
   (void)hipGetLastError();
-  hipLaunchKernelGGL(attn_split_kernel<D>, dim3((unsigned)items), dim3(kWaves * 64), lds, stream, args);
+  hipLaunchKernelGGL((attn_split_kernel<D, kLocal>), dim3((unsigned)items), dim3(kWaves * 64), lds, stream, args);
   if (plan.max_splits > 1)
     hipLaunchKernelGGL(attn_merge_kernel<D>, dim3((unsigned)units), dim3(kMergeThreads), 0, stream, args);
   const hipError_t e = hipGetLastError();
@@ -671,7 +710,7 @@ oda_status launch(const AttnArgs& args, const Plan& plan, hipStream_t stream) {
   return ODA_OK;
 }
 
-oda_status run_attention(const oda_attn_shape* s, const oda_attn_inputs* in, int n_sink, int window,
+oda_status run_attention(const oda_attn_shape* s, const oda_attn_inputs* in, bool local, int n_sink, int window,
                          int select, const int32_t* flags, const int32_t* work_list, const int32_t* n_work,
                          float* out, float* lse, void* ws, size_t ws_bytes, hipStream_t stream) {
   Plan plan;
@@ -709,9 +748,15 @@ oda_status run_attention(const oda_attn_shape* s, const oda_attn_inputs* in, int
   a.has_cur = in->k_cur != nullptr;
   a.bps = plan.bps;
   a.max_splits = plan.max_splits;
+  a.dyn_splits = plan.dyn;
+  a.nvb_max = plan.nvb_max;
   a.select = select;
   a.scale_log2 = in->scale * kLog2e;
-  oda_status st = s->head_dim == 128 ? launch<128>(a, plan, stream) : launch<64>(a, plan, stream);
+  oda_status st;
+  if (s->head_dim == 128)
+    st = local ? launch<128, true>(a, plan, stream) : launch<128, false>(a, plan, stream);
+  else
+    st = local ? launch<64, true>(a, plan, stream) : launch<64, false>(a, plan, stream);
   if (st != ODA_OK) return st;
   return oda::ok();
 }
@@ -739,7 +784,7 @@ extern "C" oda_status oda_local_decode_attn(const oda_attn_shape* shape, const o
   if (st != ODA_OK) return st;
   if (n_sink < 0) return oda::fail(ODA_ERR_SHAPE, "n_sink must be >= 0");
   if (window < 1) return oda::fail(ODA_ERR_SHAPE, "window must be >= 1 for Local attention");
-  return run_attention(shape, in, n_sink, window, kSelAll, nullptr, nullptr, nullptr, out, lse, workspace,
+  return run_attention(shape, in, true, n_sink, window, kSelAll, nullptr, nullptr, nullptr, out, lse, workspace,
                        workspace_bytes, stream);
 }
 
@@ -756,6 +801,6 @@ extern "C" oda_status oda_full_decode_attn(const oda_attn_shape* shape, const od
   if ((work_list == nullptr) != (n_work == nullptr))
     return oda::fail(ODA_ERR_NULL, "work_list and n_work must both be NULL or both be set");
   const int select = work_list ? kSelList : (flags ? kSelFlags : kSelAll);
-  return run_attention(shape, in, 0, native_window, select, flags, work_list, n_work, out, lse, workspace,
+  return run_attention(shape, in, false, 0, native_window, select, flags, work_list, n_work, out, lse, workspace,
                        workspace_bytes, stream);
 }

@@ -27,7 +27,7 @@ namespace {
 constexpr int kBatchTile = 8;     // requests per wavefront
 constexpr int kWaves = 4;         // wavefronts per workgroup
 
-enum Mode { kTower = 0, kMlpHidden = 1, kFusion = 2, kGateUp = 3, kDown = 4 };
+enum Mode { kTower = 0, kMlpHidden = 1, kGateUp = 3, kDown = 4 };
 
 struct LinArgs {
   const float* W;        // [rows][K] (kTower: tower 0's weight; the others follow at w_stride)
@@ -35,7 +35,7 @@ struct LinArgs {
   const float* bias;     // [rows] or per tower at w_stride
   const float* gain;     // RMSNorm gain [K] (kTower: per tower at w_stride; kGateUp)
   const float* X[3];     // inputs [B][K] (kTower: three; else X[0])
-  const float* aux;      // kFusion: tower outputs [3][B][dt]; kDown: residual [B][rows]
+  const float* aux;      // fusion: tower outputs [3][B][dt]; kDown: residual [B][rows]
   float* Y;              // outputs
   int64_t w_stride;      // kTower: floats between the towers' parameter segments
   int rows, K, B, dt;
@@ -55,26 +55,6 @@ __device__ __forceinline__ float4 absdiff4(float4 a, float4 b) {
   return make_float4(fabsf(a.x - b.x), fabsf(a.y - b.y), fabsf(a.z - b.z), fabsf(a.w - b.w));
 }
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
-
-// Interaction vector u = [a; b; c; a*b; |a-b|; a*c; |a-c|; b*c; |b-c|]
-// (App. A.2), four consecutive entries starting at k (all in one part).
-__device__ __forceinline__ float4 interaction4(const float* abc, int B, int dt, int b, int k) {
-  const int part = k / dt, m = k - part * dt;
-  const float4 a = *reinterpret_cast<const float4*>(abc + ((int64_t)0 * B + b) * dt + m);
-  const float4 bb = *reinterpret_cast<const float4*>(abc + ((int64_t)1 * B + b) * dt + m);
-  const float4 c = *reinterpret_cast<const float4*>(abc + ((int64_t)2 * B + b) * dt + m);
-  switch (part) {
-    case 0: return a;
-    case 1: return bb;
-    case 2: return c;
-    case 3: return mul4(a, bb);
-    case 4: return absdiff4(a, bb);
-    case 5: return mul4(a, c);
-    case 6: return absdiff4(a, c);
-    case 7: return mul4(bb, c);
-    default: return absdiff4(bb, c);
-  }
-}
 
 template <int MODE>
 __global__ __launch_bounds__(256) void gate_linear_kernel(LinArgs p) {
@@ -118,12 +98,7 @@ __global__ __launch_bounds__(256) void gate_linear_kernel(LinArgs p) {
     for (int bi = 0; bi < kBatchTile; ++bi) {
       if (bi < nb) {
         const int b = b0 + bi;
-        float4 x;
-        if (MODE == kFusion) {
-          x = interaction4(p.aux, p.B, p.dt, b, k);
-        } else {
-          x = *reinterpret_cast<const float4*>(X + (int64_t)b * p.K + k);
-        }
+        const float4 x = *reinterpret_cast<const float4*>(X + (int64_t)b * p.K + k);
         if (kNorm) ss[bi] += dot4(x, x);
         const float4 xg = kNorm ? mul4(x, gk) : x;
         acc[bi] += dot4(w, xg);
@@ -159,16 +134,62 @@ __global__ __launch_bounds__(256) void gate_linear_kernel(LinArgs p) {
     p.Y[((int64_t)tower * p.B + b) * p.dt + row] = silu(mine * inv + bias[row]);
   } else if (MODE == kMlpHidden) {
     p.Y[(int64_t)b * p.rows + row] = gelu(mine + bias[row]);
-  } else if (MODE == kFusion) {
-    const float* abc = p.aux;
-    const float s3 = abc[((int64_t)0 * p.B + b) * p.dt + row] + abc[((int64_t)1 * p.B + b) * p.dt + row] +
-                     abc[((int64_t)2 * p.B + b) * p.dt + row];
-    p.Y[(int64_t)b * p.rows + row] = 0.5f * (s3 + silu(mine + bias[row]));
   } else if (MODE == kGateUp) {
     p.Y[(int64_t)b * p.rows + row] = silu(mine * inv) * (mine2 * inv);
   } else {  // kDown
     p.Y[(int64_t)b * p.rows + row] = p.aux[(int64_t)b * p.rows + row] + mine;
   }
+}
+
+// Fusion layer of App. A.2: z0 = (a + b + c + SiLU(W_f u + b_f)) / 2 with the
+// interaction vector u = [a; b; c; a*b; |a-b|; a*c; |a-c|; b*c; |b-c|].  One
+// wavefront per (output row, batch tile); lanes walk the tower index m four at
+// a time and build the nine parts of u for those m in registers, so u is never
+// stored and W_f's nine column blocks are read with coalesced 16-byte loads.
+__global__ __launch_bounds__(256) void gate_fusion_kernel(LinArgs p) {
+  const int lane = threadIdx.x & 63;
+  const int wave = uniform(threadIdx.x >> 6);
+  const int gw = blockIdx.x * kWaves + wave;
+  const int row = gw % p.rows;
+  const int b0 = (gw / p.rows) * kBatchTile;
+  if (b0 >= p.B) return;
+  const int nb = min(kBatchTile, p.B - b0);
+  const int dt = p.dt;
+  const float* wrow = p.W + (int64_t)row * 9 * dt;
+  const float* abc = p.aux;
+  float acc[kBatchTile];
+#pragma unroll
+  for (int bi = 0; bi < kBatchTile; ++bi) acc[bi] = 0.f;
+  for (int m = 4 * lane; m < dt; m += 256) {
+    float4 w[9];
+#pragma unroll
+    for (int part = 0; part < 9; ++part) w[part] = *reinterpret_cast<const float4*>(wrow + part * dt + m);
+#pragma unroll
+    for (int bi = 0; bi < kBatchTile; ++bi) {
+      if (bi < nb) {
+        const int b = b0 + bi;
+        const float4 a = *reinterpret_cast<const float4*>(abc + ((int64_t)0 * p.B + b) * dt + m);
+        const float4 bb = *reinterpret_cast<const float4*>(abc + ((int64_t)1 * p.B + b) * dt + m);
+        const float4 c = *reinterpret_cast<const float4*>(abc + ((int64_t)2 * p.B + b) * dt + m);
+        acc[bi] += dot4(w[0], a) + dot4(w[1], bb) + dot4(w[2], c) + dot4(w[3], mul4(a, bb)) +
+                   dot4(w[4], absdiff4(a, bb)) + dot4(w[5], mul4(a, c)) + dot4(w[6], absdiff4(a, c)) +
+                   dot4(w[7], mul4(bb, c)) + dot4(w[8], absdiff4(bb, c));
+      }
+    }
+  }
+  float mine = 0.f;
+#pragma unroll
+  for (int bi = 0; bi < kBatchTile; ++bi) {
+    if (bi < nb) {
+      const float v = wave_sum(acc[bi]);
+      if (lane == bi) mine = v;
+    }
+  }
+  if (lane >= nb) return;
+  const int b = b0 + lane;
+  const float s3 = abc[((int64_t)0 * p.B + b) * dt + row] + abc[((int64_t)1 * p.B + b) * dt + row] +
+                   abc[((int64_t)2 * p.B + b) * dt + row];
+  p.Y[(int64_t)b * p.rows + row] = 0.5f * (s3 + silu(mine + p.bias[row]));
 }
 
 struct FinalArgs {
@@ -230,7 +251,8 @@ __global__ __launch_bounds__(64) void gate_final_kernel(FinalArgs p) {
   }
   if (lane == 0) {
     if (p.n_work) p.n_work[0] = total;
-    if (p.counter) p.counter[0] += total;
+    // integer add at the memory side: no round trip before the kernel can retire
+    if (p.counter) atomicAdd(reinterpret_cast<unsigned long long*>(p.counter), (unsigned long long)total);
   }
 }
 
@@ -402,7 +424,10 @@ extern "C" oda_status oda_recall_gate(const oda_gate_desc* gate, int32_t batch, 
     a.Y = z0;
     a.rows = dt;
     a.K = 9 * dt;
-    launch_linear<kFusion>(a, stream);
+    {
+      const int waves = a.rows * (int)oda::ceil_div(a.B, kBatchTile);
+      hipLaunchKernelGGL(gate_fusion_kernel, dim3((unsigned)oda::ceil_div(waves, kWaves)), dim3(256), 0, stream, a);
+    }
     // two pre-RMSNorm residual SwiGLU blocks
     float* zin = z0;
     float* zout = z1;

@@ -1,0 +1,136 @@
+"""Parity at the measured configurations' full sizes, in the launch
+configuration bench.py times (stacked calls, automatic work plan): one decode
+step on the GPU, then sampled (layer, request) rows recomputed by the fp64
+oracle from copies of exactly the blocks those rows read.  Gate scores and
+flags are compared for every request."""
+import gc
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from harness import FLAG_BORDER, check_close
+from oracle import attention as OA
+from oracle import gate as OG
+
+pytestmark = pytest.mark.gpu
+
+
+def _bench(name, head="paper"):
+    import bench as BN
+    from paper_2609_20734_amd import workloads as WL
+    return BN.Bench(WL.ALL[name], head, 1234, 1)
+
+
+def _host_slice(b, st, layer, req):
+    """Host copies of one request's blocks of one layer, with a renumbered table."""
+    n = int(b.seq_host[req])
+    nblk = (n + 15) // 16
+    phys = b.dtable[req, :nblk].long()
+    k = st.k[layer].index_select(0, phys).cpu().view(torch.int16).numpy().view(np.uint16)[None]
+    v = st.v[layer].index_select(0, phys).cpu().view(torch.int16).numpy().view(np.uint16)[None]
+    q = st.q[layer:layer + 1, req:req + 1].cpu().numpy().view(np.uint16)
+    table = np.arange(nblk, dtype=np.int32)[None, :]
+    return q, k, v, table, np.array([n], dtype=np.int32)
+
+
+def _run_step(b, tau):
+    calls = b.step_calls(tau)[0]
+    for c in calls:
+        c()
+    torch.cuda.synchronize()
+
+
+def _check_gate(b, tau):
+    wl = b.wl
+    params = b.params.cpu().numpy()
+    h, e, l = (x[0].cpu().numpy().astype(np.float64) for x in (b.h, b.e, b.l))
+    if b.head == "paper":
+        ref = OG.paper_head_score(params, wl.d_model, wl.d_hidden, 1e-6, h, e, l)
+    else:
+        ref = OG.mlp_score(params, wl.d_model, wl.d_hidden, l)
+    sc = b.score.cpu().numpy()
+    assert np.max(np.abs(sc - ref)) <= 1e-4 * max(1.0, float(np.max(np.abs(ref))))
+    flags = b.flags.cpu().numpy().astype(bool)
+    want = OG.decide(ref, tau)
+    border = np.abs(ref - tau) < FLAG_BORDER
+    assert not np.any((flags != want) & ~border)
+    n = int(b.n_work.item())
+    assert n == int(flags.sum()) and np.array_equal(b.work.cpu().numpy()[:n], np.flatnonzero(flags))
+    return flags
+
+
+def _check_rows(b, flags, samples):
+    for si, layer, req in samples:
+        st = b.stacks[si]
+        q, k, v, table, seq = _host_slice(b, st, layer, req)
+        if flags[req]:
+            f = lambda n: OA.native_window_set(n, st.stack.native_window)
+        elif st.stack.gated:
+            f = lambda n: OA.local_set(n, st.stack.local_sink, st.stack.local_window)
+        else:
+            f = lambda n: OA.native_window_set(n, st.stack.native_window)
+        ref, lse_ref, _ = OA.decode_attention(q, k, v, table, seq, f, 1.0 / math.sqrt(b.wl.head_dim))
+        got = st.out[layer, req].cpu().numpy()
+        check_close(got, ref[0, 0], what=f"{st.stack.name} layer {layer} request {req}")
+        assert np.max(np.abs(st.lse[layer, req].cpu().numpy() - lse_ref[0, 0])) < 1e-4
+
+
+def _median_tau(b):
+    sc = b.scores()[0]
+    s = np.sort(sc)
+    if len(s) == 1:
+        return None
+    m = len(s) // 2
+    return float(0.5 * (s[m - 1] + s[m]))
+
+
+@pytest.fixture(autouse=True)
+def _release_memory():
+    yield
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def test_llama_full_size():
+    b = _bench("llama3-8b")
+    for tau in (math.inf, -math.inf):
+        _run_step(b, tau)
+        flags = _check_gate(b, tau)
+        _check_rows(b, flags, [(0, 0, 0), (0, 17, 0), (0, 31, 0)])
+
+
+def test_long_full_size():
+    b = _bench("long")
+    tau = _median_tau(b)
+    _run_step(b, tau)
+    flags = _check_gate(b, tau)
+    assert 0 < flags.sum() < b.wl.batch
+    on = int(np.flatnonzero(flags)[0])
+    off = int(np.flatnonzero(~flags)[0])
+    _check_rows(b, flags, [(0, 0, on), (0, 31, off), (0, 13, on)])
+
+
+def test_mixed_full_size():
+    b = _bench("mixed")
+    tau = _median_tau(b)
+    _run_step(b, tau)
+    flags = _check_gate(b, tau)
+    on = np.flatnonzero(flags)
+    off = np.flatnonzero(~flags)
+    lens = b.seq_host
+    longest_on = int(on[np.argmax(lens[on])])
+    shortest_off = int(off[np.argmin(lens[off])])
+    _check_rows(b, flags, [(0, 0, longest_on), (0, 31, shortest_off), (0, 5, int(on[0]))])
+
+
+def test_hybrid_full_size():
+    b = _bench("hybrid")
+    tau = _median_tau(b)
+    _run_step(b, tau)
+    flags = _check_gate(b, tau)
+    on = int(np.flatnonzero(flags)[0])
+    off = int(np.flatnonzero(~flags)[0])
+    # stack 0: native sliding-window layers; stack 1: global, ODA-gated layers
+    _check_rows(b, flags, [(0, 0, off), (0, 35, on), (1, 0, on), (1, 11, off)])

@@ -1,0 +1,43 @@
+"""The bench's closed-form byte ledger agrees with the oracle's ledger (which
+counts the attended positions of the access sets directly), and the closed
+forms reproduce hand-computable sizes of the measured configurations."""
+import numpy as np
+import pytest
+
+from oracle import ledger as OL
+from paper_2609_20734_amd import ledger as PL
+from paper_2609_20734_amd import workloads as WL
+
+
+@pytest.mark.parametrize("n,s,w", [(1, 4, 16), (5, 4, 3), (20, 0, 5), (2052, 4, 2048), (2053, 4, 2048),
+                                   (32768, 4, 1024), (33, 16, 16), (100, 40, 50), (7, 4, 0)])
+def test_local_count_matches_set_size(n, s, w):
+    from oracle import attention as OA
+    ref = len(OA.local_set(n, s, w)) if w > 0 else n
+    assert PL.local_count(n, s, w) == ref
+    blocks = len(np.unique(OA.local_set(n, s, w) // 16)) if w > 0 else (n + 15) // 16
+    assert PL.visited_blocks(n, s, w) == blocks
+
+
+def test_attention_bytes_match_oracle_ledger():
+    seq = [1, 17, 300, 2049, 5000]
+    from oracle import attention as OA
+    for s, w in ((4, 1024), (0, 64), (4, 0)):
+        a = PL.attention_bytes(seq, s, w, 3, 16, 4, 128)
+        f = (lambda n: OA.local_set(n, s, w)) if w > 0 else OA.full_set
+        b = OL.attention_bytes(seq, f, 3, 16, 4, 128)
+        assert a == b
+
+
+def test_gate_bytes_match_oracle_ledger():
+    for kind, d, dh in (("paper", 4096, 256), ("mlp", 4096, 256), ("paper", 8192, 512)):
+        assert PL.gate_bytes(kind, 8, d, dh) == OL.gate_bytes(kind, 8, d, dh)
+    assert PL.gate_param_count("paper", 2048, 1024) == 28_325_889
+
+
+def test_llama_config_sizes():
+    wl = WL.LLAMA
+    full = PL.attention_bytes(wl.seq_lens, 0, 0, 32, 32, 8, 128)
+    assert full["kv"] == 32 * 8 * 32768 * 4 * 128 == 4_294_967_296
+    loc = PL.attention_bytes(wl.seq_lens, 4, 1024, 32, 32, 8, 128)
+    assert loc["kv"] == 32 * 8 * 1028 * 512
