@@ -104,7 +104,7 @@ class Bench:
 
         import oda_synth as S
         import paper_2609_20734_amd as P
-        self.P, self.torch, self.wl, self.head, self.seed, self.K = P, torch, wl, head, seed, steps
+        self.P, self.torch, self.wl, self.seed, self.K = P, torch, wl, seed, steps
         dev = torch.device("cuda:0")
         self.dev = dev
         B = wl.batch
@@ -125,15 +125,11 @@ class Bench:
         self.stacks = [StackState(P, wl, st, self.dseq, self.dtable, nb, mb, seed, dev, split_blocks)
                        for st in wl.stacks]
         # gate
-        kind = P.HEAD_PAPER if head == "paper" else P.HEAD_MLP
-        params = S.gate_params(seed, head, wl.d_model, wl.d_hidden)
-        self.params = torch.from_numpy(params).to(dev)
-        self.gate = P.gate_desc(kind, wl.d_model, wl.d_hidden, self.params, 1e-6)
         h, e, l = S.gate_inputs(seed, steps, B, wl.d_model)
         self.h = torch.from_numpy(h).to(dev)
         self.e = torch.from_numpy(e).to(dev)
         self.l = torch.from_numpy(l).to(dev)
-        self.ws_gate = torch.empty(P.gate_workspace_size(self.gate, B), dtype=torch.uint8, device=dev)
+        self.set_head(head)
         self.score = torch.zeros(B, dtype=torch.float32, device=dev)
         self.flags = torch.zeros(B, dtype=torch.int32, device=dev)
         self.work = torch.zeros(B, dtype=torch.int32, device=dev)
@@ -145,6 +141,19 @@ class Bench:
 
     def flush(self):
         self.flush_buf.max()
+
+    def set_head(self, head):
+        """Recall head used by the steps: the App. A.2 form ("paper") or the MLP stand-in."""
+        import torch
+
+        import oda_synth as S
+        P, wl = self.P, self.wl
+        self.head = head
+        kind = P.HEAD_PAPER if head == "paper" else P.HEAD_MLP
+        params = S.gate_params(self.seed, head, wl.d_model, wl.d_hidden)
+        self.params = torch.from_numpy(params).to(self.dev)
+        self.gate = P.gate_desc(kind, wl.d_model, wl.d_hidden, self.params, 1e-6)
+        self.ws_gate = torch.empty(P.gate_workspace_size(self.gate, wl.batch), dtype=torch.uint8, device=self.dev)
 
     # -- calls ---------------------------------------------------------------
     def step_calls(self, tau, forced=None):
@@ -303,6 +312,49 @@ def cpu_baseline(b, rho, budget_s=15.0):
                 measured_s=t_gate + t_local + t_full)
 
 
+def run_sweep(b, wl, args, full_us):
+    """Time the step over the configuration's recall rates (threshold-driven) or
+    Bernoulli schedules (forced flags, gate still run); one entry per point."""
+    import torch
+    K = b.K
+    local_b, gate_b, full_b = bytes_for(wl, b.seq_host, None, b.head)
+    bytes_full = sum(full_b)
+    sweep = []
+    if wl.rhos:
+        sc = b.scores()
+        taus = taus_for(sc, wl.rhos)
+        points = [(rho, taus[rho], None, None) for rho in wl.rhos]
+    else:
+        import oda_synth as S
+        points = []
+        for p in wl.bernoulli:
+            forced_np = S.bernoulli_flags(args.seed, K, wl.batch, p)
+            points.append((p, 0.0, torch.from_numpy(forced_np).to(b.dev), forced_np))
+    for rho, tau, forced, forced_np in points:
+        r = b.timed(b.step_calls(tau, forced=forced), args.warmup, cold=True)
+        real = r["recalled"] / (K * wl.batch)
+        if forced_np is None:
+            full_part = real * bytes_full
+        else:
+            full_part = float(np.mean([(forced_np[t] * np.array(full_b)).sum() for t in range(K)]))
+        step_bytes = local_b + gate_b + full_part
+        ent = dict(rho=rho, realised_rho=real, us=r["us_mean"], us_median=r["us_median"], us_min=r["us_min"],
+                   us_max=r["us_max"], GBps=step_bytes / r["us_mean"] / 1e3, ratio=r["us_mean"] / full_us,
+                   ideal_ratio=step_bytes / bytes_full)
+        if forced_np is None:
+            ent["tau"] = tau
+        ent["hbm_frac"] = ent["GBps"] / HBM_PEAK_GBS
+        ent["linearity"] = ent["ratio"] / ent["ideal_ratio"]
+        if args.warm:
+            w = b.timed(b.step_calls(tau, forced=forced), args.warmup, cold=False)
+            ent["warm_us"] = w["us_mean"]
+            ent["warm_bracket_us"] = w["bracket_us"]
+        sweep.append(ent)
+        log(f"[bench] {b.head} head rho={rho:.3f} (real {real:.3f}) {r['us_mean']:.1f} us/step ratio {ent['ratio']:.3f} "
+            f"ideal {ent['ideal_ratio']:.3f} x{ent['linearity']:.2f} {ent['GBps']:.0f} GB/s")
+    return sweep
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -314,6 +366,7 @@ def main():
     ap.add_argument("--split-blocks", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--warm", action="store_true", help="also time back-to-back (warm) steps")
+    ap.add_argument("--one-head", action="store_true", help="skip the second recall head's sweep")
     ap.add_argument("--roofline-only", action="store_true",
                     help="only the roofline leg (always-Full calls) plus a 1 GiB copy, for PMC profiling")
     args = ap.parse_args()
@@ -348,42 +401,15 @@ def main():
     full = b.timed(b.full_calls(), args.warmup, cold=True)
     log(f"[bench] always-Full {full['us_mean']:.1f} us/step ({bytes_full / full['us_mean'] / 1e3:.0f} GB/s)")
 
-    # rho sweep
-    sweep = []
-    if wl.rhos:
-        sc = b.scores()
-        taus = taus_for(sc, wl.rhos)
-        for rho in wl.rhos:
-            r = b.timed(b.step_calls(taus[rho]), args.warmup, cold=True)
-            real = r["recalled"] / (K * wl.batch)
-            step_bytes = local_b + gate_b + real * bytes_full
-            ent = dict(rho=rho, tau=taus[rho], realised_rho=real, us=r["us_mean"], us_median=r["us_median"],
-                       us_min=r["us_min"], us_max=r["us_max"], GBps=step_bytes / r["us_mean"] / 1e3,
-                       ratio=r["us_mean"] / full["us_mean"], ideal_ratio=step_bytes / bytes_full)
-            ent["linearity"] = ent["ratio"] / ent["ideal_ratio"]
-            if args.warm:
-                w = b.timed(b.step_calls(taus[rho]), args.warmup, cold=False)
-                ent["warm_us"] = w["us_mean"]
-                ent["warm_bracket_us"] = w["bracket_us"]
-            sweep.append(ent)
-            log(f"[bench] rho={rho:.3f} (real {real:.3f}) {r['us_mean']:.1f} us/step ratio {ent['ratio']:.3f} "
-                f"ideal {ent['ideal_ratio']:.3f} x{ent['linearity']:.2f} {ent['GBps']:.0f} GB/s")
-    else:
-        import oda_synth as S
-        for p in wl.bernoulli:
-            forced_np = S.bernoulli_flags(args.seed, K, wl.batch, p)
-            forced = torch.from_numpy(forced_np).to(b.dev)
-            r = b.timed(b.step_calls(0.0, forced=forced), args.warmup, cold=True)
-            real = r["recalled"] / (K * wl.batch)
-            exp_full = float(np.mean([(forced_np[t] * np.array(full_b)).sum() for t in range(K)]))
-            step_bytes = local_b + gate_b + exp_full
-            ent = dict(rho=p, realised_rho=real, us=r["us_mean"], us_median=r["us_median"], us_min=r["us_min"],
-                       us_max=r["us_max"], GBps=step_bytes / r["us_mean"] / 1e3, ratio=r["us_mean"] / full["us_mean"],
-                       ideal_ratio=step_bytes / bytes_full)
-            ent["linearity"] = ent["ratio"] / ent["ideal_ratio"]
-            sweep.append(ent)
-            log(f"[bench] p={p:.2f} (real {real:.3f}) {r['us_mean']:.1f} us/step ratio {ent['ratio']:.3f} "
-                f"ideal {ent['ideal_ratio']:.3f} x{ent['linearity']:.2f}")
+    # rho sweep with the App. A.2 head (headline), then the MLP stand-in
+    head0 = args.head
+    sweep = run_sweep(b, wl, args, full["us_mean"])
+    other = "mlp" if head0 == "paper" else "paper"
+    sweep_other = []
+    if not args.one_head:
+        b.set_head(other)
+        sweep_other = run_sweep(b, wl, args, full["us_mean"])
+        b.set_head(head0)
 
     # roofline of the dominant kernel: the Full split-K pass over every request
     # (one launch of attn_split_kernel<128, false>; no merge launch at this size),
@@ -414,6 +440,8 @@ def main():
         "always_full_us": round(full["us_mean"], 3),
         "always_full_GBps": round(bytes_full / full["us_mean"] / 1e3, 1),
         "sweep": [{k: (round(v, 4) if isinstance(v, float) else v) for k, v in e.items()} for e in sweep],
+        f"sweep_{other}_head": [{k: (round(v, 4) if isinstance(v, float) else v) for k, v in e.items()}
+                                for e in sweep_other],
         "roofline": {k: (round(v, 4) if isinstance(v, float) else v) for k, v in roof.items()},
     }
     if not args.no_cpu_baseline:
