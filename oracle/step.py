@@ -39,3 +39,19 @@ def decode_step(q, k_cache, v_cache, block_table, seq_lens, scale, n_sink, windo
     return dict(out_local=local[0], lse_local=local[1], count_local=local[2],
                 score=score, flags=flags.astype(np.int32), work_list=work, n_work=n_work,
                 out_full=full[0], lse_full=full[1], out=out, lse=lse)
+
+
+def commit(k_cache, v_cache, block_table, seq_lens, k_local, v_local, k_full, v_full, flags):
+    """C_t = C_{t-1} || dC_t^{b_t} (App. A.5, commit equation), in place on host
+    copies: the selected branch's candidate K/V of every layer goes to position
+    n_b - 1 of request b; then every n_b advances by one.  Pure data movement."""
+    L, B, Hkv, D = k_local.shape
+    for b in range(B):
+        pos = int(seq_lens[b]) - 1
+        phys = int(block_table[b, pos // 16])
+        ks, vs = (k_full, v_full) if flags[b] else (k_local, v_local)
+        for l in range(L):
+            for g in range(Hkv):
+                k_cache[l, phys, g, :, pos % 16, :] = ks[l, b, g].reshape(D // 8, 8)
+                v_cache[l, phys, g, :, pos % 16] = vs[l, b, g]
+        seq_lens[b] += 1

@@ -13,7 +13,7 @@ not been built that raises ImportError (there is no fallback path).
 """
 _EXPORTS = ("HEAD_MLP", "HEAD_PAPER", "OdaError", "Shape", "attn_workspace_size", "full_decode_attn",
             "gate_desc", "gate_param_count", "gate_workspace_size", "inputs", "local_decode_attn",
-            "recall_gate", "lib", "prepare_local", "prepare_full", "prepare_gate", "Call")
+            "recall_gate", "lib", "prepare_local", "prepare_full", "prepare_gate", "Call", "commit_kv", "prepare_commit")
 
 
 def __getattr__(name):

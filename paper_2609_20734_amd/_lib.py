@@ -31,7 +31,7 @@ HEAD_PAPER = 0
 HEAD_MLP = 1
 
 EXPORTED = ("oda_attn_workspace_size", "oda_local_decode_attn", "oda_full_decode_attn",
-            "oda_gate_param_count", "oda_gate_workspace_size", "oda_recall_gate",
+            "oda_gate_param_count", "oda_gate_workspace_size", "oda_recall_gate", "oda_commit_kv",
             "oda_status_string", "oda_last_error")
 
 
@@ -82,6 +82,10 @@ _lib.oda_recall_gate.argtypes = [_P(GateDesc), ctypes.c_int32, ctypes.c_void_p, 
                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                  ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
 _lib.oda_recall_gate.restype = ctypes.c_int
+_lib.oda_commit_kv.argtypes = [_P(AttnShape), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                               ctypes.c_int32, ctypes.c_void_p]
+_lib.oda_commit_kv.restype = ctypes.c_int
 _lib.oda_status_string.argtypes = [ctypes.c_int]
 _lib.oda_status_string.restype = ctypes.c_char_p
 _lib.oda_last_error.argtypes = []
@@ -205,6 +209,13 @@ def recall_gate(gate: GateDesc, batch: int, h_prev, emb, h_local, tau: float, fo
                                 _ptr(n_work), _ptr(recall_counter), _ptr(workspace), wb, _stream(stream)))
 
 
+def commit_kv(shape: Shape, k_cache, v_cache, block_table, seq_lens, k_local, v_local, k_full=None, v_full=None,
+              flags=None, advance: bool = True, stream=None) -> None:
+    _check(_lib.oda_commit_kv(ctypes.byref(shape.c()), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+                              _ptr(seq_lens), _ptr(k_local), _ptr(v_local), _ptr(k_full), _ptr(v_full),
+                              _ptr(flags), 1 if advance else 0, _stream(stream)))
+
+
 # ---------------------------------------------------------------------------
 # pre-marshalled calls (for tight launch loops: no per-call conversion)
 # ---------------------------------------------------------------------------
@@ -251,3 +262,12 @@ def prepare_gate(gate: GateDesc, batch: int, h_prev, emb, h_local, tau: float, f
             _nbytes(workspace, workspace_bytes), _stream(stream))
     return Call(_lib.oda_recall_gate, args, (gate, h_prev, emb, h_local, forced, score, flags, work_list, n_work,
                                             recall_counter, workspace))
+
+
+def prepare_commit(shape: Shape, k_cache, v_cache, block_table, seq_lens, k_local, v_local, k_full=None,
+                   v_full=None, flags=None, advance: bool = True, stream=None) -> Call:
+    cs = shape.c()
+    args = (ctypes.byref(cs), _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(seq_lens), _ptr(k_local),
+            _ptr(v_local), _ptr(k_full), _ptr(v_full), _ptr(flags), 1 if advance else 0, _stream(stream))
+    return Call(_lib.oda_commit_kv, args, (cs, k_cache, v_cache, block_table, seq_lens, k_local, v_local, k_full,
+                                          v_full, flags))

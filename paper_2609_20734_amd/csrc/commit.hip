@@ -1,0 +1,111 @@
+// Selected-state commit (App. A.5, commit equation): the chosen branch's
+// current-position K/V of every layer is appended to the paged cache in one
+// launch, then the request's length advances.  One workgroup per request:
+// it reads seq_lens[b] before any thread of it advances it, so no other
+// workgroup can observe a half-advanced length.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "oda.h"
+#include "oda_internal.h"
+
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kBlock = 16;
+constexpr int kThreads = 256;
+
+struct CommitArgs {
+  uint16_t* k_cache;
+  uint16_t* v_cache;
+  const int32_t* block_table;
+  int32_t* seq_lens;
+  const uint16_t* k_local;
+  const uint16_t* v_local;
+  const uint16_t* k_full;
+  const uint16_t* v_full;
+  const int32_t* flags;
+  int64_t kv_layer_stride;   // elements between layers of the caches
+  int32_t L, B, Hkv, D, MB;
+  int32_t advance;
+};
+
+__global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
+  const int b = blockIdx.x;
+  const int n = a.seq_lens[b];
+  const int pos = n - 1;
+  const bool full = a.flags != nullptr && a.flags[b] != 0;
+  const uint16_t* ks = full ? a.k_full : a.k_local;
+  const uint16_t* vs = full ? a.v_full : a.v_local;
+  const int64_t blk = a.block_table[(int64_t)b * a.MB + pos / kBlock];
+  const int slot = pos % kBlock;
+  const int groups = a.D / 8;                       // 16-byte groups of 8 dims
+  const int64_t head_elems = (int64_t)kBlock * a.D;
+  const int64_t total = (int64_t)a.L * a.Hkv * groups;
+  for (int64_t i = threadIdx.x; i < total; i += kThreads) {
+    const int d8 = (int)(i % groups);
+    const int64_t lg = i / groups;
+    const int g = (int)(lg % a.Hkv);
+    const int l = (int)(lg / a.Hkv);
+    const int64_t src = (((int64_t)l * a.B + b) * a.Hkv + g) * a.D + d8 * 8;
+    const int64_t base = (int64_t)l * a.kv_layer_stride + (blk * a.Hkv + g) * head_elems;
+    // K block [D/8][16][8]: the 8 dims are one 16-byte group
+    *reinterpret_cast<u32x4*>(a.k_cache + base + ((int64_t)d8 * kBlock + slot) * 8) =
+        *reinterpret_cast<const u32x4*>(ks + src);
+    // V block [D][16]: dim d sits at d * 16 + slot
+    const u32x4 v = *reinterpret_cast<const u32x4*>(vs + src);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint16_t x = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
+      a.v_cache[base + (int64_t)(d8 * 8 + e) * kBlock + slot] = x;
+    }
+  }
+  __syncthreads();
+  if (a.advance && threadIdx.x == 0) a.seq_lens[b] = n + 1;
+}
+
+}  // namespace
+
+extern "C" oda_status oda_commit_kv(const oda_attn_shape* shape, uint16_t* k_cache, uint16_t* v_cache,
+                                   const int32_t* block_table, int32_t* seq_lens, const uint16_t* k_local,
+                                   const uint16_t* v_local, const uint16_t* k_full, const uint16_t* v_full,
+                                   const int32_t* flags, int32_t advance, hipStream_t stream) {
+  if (shape == nullptr) return oda::fail(ODA_ERR_NULL, "shape is NULL");
+  if (!k_cache || !v_cache || !block_table || !seq_lens || !k_local || !v_local)
+    return oda::fail(ODA_ERR_NULL, "k_cache, v_cache, block_table, seq_lens, k_local and v_local are required");
+  if ((k_full == nullptr) != (v_full == nullptr))
+    return oda::fail(ODA_ERR_NULL, "k_full and v_full must both be NULL or both be set");
+  if (shape->num_layers < 1 || shape->batch < 1 || shape->num_kv_heads < 1 || shape->num_blocks < 1 ||
+      shape->max_blocks_per_seq < 1)
+    return oda::fail(ODA_ERR_SHAPE, "num_layers, batch, num_kv_heads, num_blocks, max_blocks_per_seq must be >= 1");
+  if (shape->head_dim != 64 && shape->head_dim != 128)
+    return oda::fail(ODA_ERR_UNSUPPORTED, "head_dim %d not in {64, 128}", shape->head_dim);
+  if (shape->block_size != kBlock) return oda::fail(ODA_ERR_UNSUPPORTED, "block_size %d != 16", shape->block_size);
+  if (!oda::aligned(k_cache, 16) || !oda::aligned(v_cache, 16) || !oda::aligned(k_local, 16) ||
+      !oda::aligned(v_local, 16) || (k_full && (!oda::aligned(k_full, 16) || !oda::aligned(v_full, 16))))
+    return oda::fail(ODA_ERR_SHAPE, "caches and candidates must be 16-byte aligned");
+  CommitArgs a;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.block_table = block_table;
+  a.seq_lens = seq_lens;
+  a.k_local = k_local;
+  a.v_local = v_local;
+  a.k_full = k_full ? k_full : k_local;
+  a.v_full = v_full ? v_full : v_local;
+  a.flags = flags;
+  a.kv_layer_stride = shape->num_blocks * shape->num_kv_heads * kBlock * shape->head_dim;
+  a.L = shape->num_layers;
+  a.B = shape->batch;
+  a.Hkv = shape->num_kv_heads;
+  a.D = shape->head_dim;
+  a.MB = shape->max_blocks_per_seq;
+  a.advance = advance != 0;
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(commit_kernel, dim3((unsigned)shape->batch), dim3(kThreads), 0, stream, a);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return oda::fail(ODA_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return oda::ok();
+}

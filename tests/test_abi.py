@@ -138,3 +138,23 @@ def test_gate_rejects_bad_arguments(L):
 def test_status_strings(L):
     for s in (0, -1, -2, -3, -4, -5):
         assert L.status_string(s).startswith("ODA_")
+
+
+def test_commit_rejects_bad_arguments(L):
+    s = _shape(L)
+    args = dict(k_cache=0x1000, v_cache=0x2000, table=0x3000, seq=0x4000, kl=0x5000, vl=0x6000)
+
+    def call(kw, shape=s):
+        a = dict(args)
+        a.update(kw)
+        L.commit_kv(shape, a["k_cache"], a["v_cache"], a["table"], a["seq"], a["kl"], a["vl"], a.get("kf"),
+                    a.get("vf"), None, True, stream=0)
+
+    for kw, status in [(dict(k_cache=None), -1), (dict(kl=None), -1), (dict(kf=0x7000), -1),
+                       (dict(kl=0x5008), -2)]:
+        with pytest.raises(L.OdaError) as e:
+            call(kw)
+        assert e.value.status == status, (kw, e.value)
+    with pytest.raises(L.OdaError) as e:
+        call({}, shape=_shape(L, head_dim=96))
+    assert e.value.status == -3

@@ -255,3 +255,33 @@ def test_current_candidate_equals_cached_current_token():
         v2[:, table[b][p // 16], :, :, p % 16] = 0x7FC0
     bres = A.decode_attention(q, k2, v2, table, seq, f, 0.2, k_cur=kc, v_cur=vc)
     np.testing.assert_allclose(bres[0], a[0], rtol=1e-12, atol=1e-14)
+
+
+def test_commit_appends_selected_candidate():
+    """App. A.5 commit equation: after committing, the cache holds the selected
+    candidate at position n-1, so attending without the candidate gives what
+    attending with it gave; the unselected branch's candidate is nowhere."""
+    from oracle import step as OS
+    q, k, v, table, seq, kc, vc = _tiny_problem(23, seq=(3, 16, 40), cur=True)
+    kf = S.normal_bf16(S.rng(99, S.STREAM_KCUR), kc.shape)
+    vf = S.normal_bf16(S.rng(99, S.STREAM_VCUR), vc.shape)
+    flags = np.array([0, 1, 0])
+    f = lambda n: A.local_set(n, 2, 9)
+    before_l = A.decode_attention(q, k, v, table, seq, f, 0.3, k_cur=kc, v_cur=vc)
+    before_f = A.decode_attention(q, k, v, table, seq, f, 0.3, k_cur=kf, v_cur=vf)
+    k2, v2, s2 = k.copy(), v.copy(), seq.copy()
+    OS.commit(k2, v2, table, s2, kc, vc, kf, vf, flags)
+    assert s2.tolist() == [4, 17, 41]
+    after = A.decode_attention(q, k2, v2, table, seq, f, 0.3)
+    for b in range(3):
+        want = before_f if flags[b] else before_l
+        np.testing.assert_array_equal(after[0][:, b], want[0][:, b])
+        p = int(seq[b]) - 1
+        src = kf if flags[b] else kc
+        assert np.array_equal(k2[:, table[b][p // 16], :, :, p % 16, :].reshape(src[:, b].shape), src[:, b])
+    # nothing else changed
+    mask = np.ones(k.shape[:2] + k.shape[2:], bool)
+    for b in range(3):
+        p = int(seq[b]) - 1
+        mask[:, table[b][p // 16], :, :, p % 16, :] = False
+    assert np.array_equal(k2[mask], k[mask])
