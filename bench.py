@@ -72,13 +72,13 @@ def log(*a):
 class StackState:
     """Device buffers of one layer group (shared block table)."""
 
-    def __init__(self, P, wl, stack, seq, table, num_blocks, mb, seed, dev, split_blocks):
+    def __init__(self, P, wl, stack, seq, table, num_blocks, mb, max_len, seed, dev, split_blocks):
         import torch
 
         import oda_synth as S
         self.stack = stack
         L, B, Hq, Hkv, D = stack.num_layers, wl.batch, wl.num_q_heads, wl.num_kv_heads, wl.head_dim
-        self.shape = P.Shape(L, B, Hq, Hkv, D, mb, int(max(seq)), num_blocks, split_blocks)
+        self.shape = P.Shape(L, B, Hq, Hkv, D, mb, max_len, num_blocks, split_blocks)
         self.k = torch.empty((L, num_blocks, Hkv, D // 8, 16, 8), dtype=torch.bfloat16, device=dev)
         self.v = torch.empty((L, num_blocks, Hkv, D, 16), dtype=torch.bfloat16, device=dev)
         S.fill_normal_bf16_(self.k, seed, S.STREAM_K + 100 * len(stack.name))
@@ -99,7 +99,7 @@ class StackState:
 
 
 class Bench:
-    def __init__(self, wl, head, seed, steps, split_blocks=0):
+    def __init__(self, wl, head, seed, steps, split_blocks=0, growth=0):
         import torch
 
         import oda_synth as S
@@ -113,8 +113,9 @@ class Bench:
         else:
             seq = S.uniform_seq_lens(seed, B, *wl.seq_range)
         self.seq_host = seq
-        mb = int(math.ceil(seq.max() / 16))
-        table, nb = S.paged_block_table(S.rng(seed, S.STREAM_TABLE), seq, mb, permute=wl.permute)
+        self.growth = growth     # positions a decode loop may append (blocks reserved in the table)
+        mb = int(math.ceil((seq.max() + growth) / 16))
+        table, nb = S.paged_block_table(S.rng(seed, S.STREAM_TABLE), seq + growth, mb, permute=wl.permute)
         need = sum(st.num_layers for st in wl.stacks) * nb * wl.num_kv_heads * wl.head_dim * 16 * 2 * 2
         free, total = torch.cuda.mem_get_info()
         log(f"[bench] {wl.name}: KV {need / 1e9:.2f} GB, device free {free / 1e9:.1f} GB")
@@ -122,8 +123,8 @@ class Bench:
             raise SystemExit(f"workload needs {need / 1e9:.1f} GB of KV, only {free / 1e9:.1f} GB free")
         self.dtable = torch.from_numpy(table).to(dev)
         self.dseq = torch.from_numpy(seq).to(dev)
-        self.stacks = [StackState(P, wl, st, self.dseq, self.dtable, nb, mb, seed, dev, split_blocks)
-                       for st in wl.stacks]
+        self.stacks = [StackState(P, wl, st, self.dseq, self.dtable, nb, mb, int(seq.max()) + growth, seed, dev,
+                                  split_blocks) for st in wl.stacks]
         # gate
         h, e, l = S.gate_inputs(seed, steps, B, wl.d_model)
         self.h = torch.from_numpy(h).to(dev)
@@ -169,6 +170,87 @@ class Bench:
                                self.flags, self.work, self.n_work, self.counter, self.ws_gate)
             steps.append(local + [g] + full)
         return steps
+
+    def decode_loop(self, firsts=(0, 2, 4, 8, 16), period=16, reps=4):
+        """The paper's runtime protocol (App. B.7) as a growing-context loop: a
+        device-side schedule selects Full for the first k of every `period`
+        steps, the gate still runs every step, and each step commits the
+        selected candidate (Local or Full current-position K/V of every layer)
+        so the context grows by one.  One period is captured as a HIP graph and
+        replayed `reps` times back to back (warm, like the paper's throughput
+        measurement); the same period launched eagerly is timed too."""
+        import oda_synth as S
+        torch, P, wl = self.torch, self.P, self.wl
+        B = wl.batch
+        assert self.growth >= period * (reps + 2), "table has no room for the loop"
+        cands = []
+        for si, st in enumerate(self.stacks):
+            shp = (period, st.stack.num_layers, B, wl.num_kv_heads, wl.head_dim)
+            c = [torch.empty(shp, dtype=torch.bfloat16, device=self.dev) for _ in range(4)]
+            for i, x in enumerate(c):
+                S.fill_normal_bf16_(x, self.seed + 17 * si + i, S.STREAM_KCUR)
+            cands.append(c)
+        scale = 1.0 / math.sqrt(wl.head_dim)
+        seq0 = self.dseq.clone()
+        res = []
+
+        def one_period(forced):
+            for t in range(period):
+                for st, (kl, vl, kf, vf) in zip(self.stacks, cands):
+                    inp = P.inputs(st.q, st.k, st.v, self.dtable, self.dseq, scale, kl[t], vl[t])
+                    P.local_decode_attn(st.shape, inp, *st.local_args, st.out, st.lse, st.ws_local)
+                P.recall_gate(self.gate, B, self.h[t % self.K], self.e[t % self.K], self.l[t % self.K], 0.0,
+                              forced[t], self.score, self.flags, self.work, self.n_work, self.counter, self.ws_gate)
+                for st, (kl, vl, kf, vf) in zip(self.stacks, cands):
+                    inp = P.inputs(st.q, st.k, st.v, self.dtable, self.dseq, scale, kf[t], vf[t])
+                    P.full_decode_attn(st.shape, inp, st.stack.native_window, None, self.work, self.n_work,
+                                       st.out, st.lse, st.ws_full)
+                for i, (st, (kl, vl, kf, vf)) in enumerate(zip(self.stacks, cands)):
+                    P.commit_kv(st.shape, st.k, st.v, self.dtable, self.dseq, kl[t], vl[t], kf[t], vf[t],
+                                self.flags, i == len(self.stacks) - 1)
+
+        for k in firsts:
+            sched = np.stack([S.periodic_schedule(period, k)] * B, axis=1).astype(np.int32)
+            forced = torch.from_numpy(sched).to(self.dev)
+            # eager: launched from the host every period
+            self.dseq.copy_(seq0)
+            one_period(forced)
+            torch.cuda.synchronize()
+            self.dseq.copy_(seq0)
+            self.counter.zero_()
+            a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(reps):
+                one_period(forced)
+            b_.record()
+            torch.cuda.synchronize()
+            eager_us = a.elapsed_time(b_) * 1e3 / (reps * period)
+            recalled = int(self.counter.item())
+            # graph: the whole period captured once, replayed
+            self.dseq.copy_(seq0)
+            g = torch.cuda.CUDAGraph()
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g):
+                one_period(forced)
+            self.dseq.copy_(seq0)
+            g.replay()
+            torch.cuda.synchronize()
+            self.dseq.copy_(seq0)
+            torch.cuda.synchronize()
+            a.record()
+            for _ in range(reps):
+                g.replay()
+            b_.record()
+            torch.cuda.synchronize()
+            graph_us = a.elapsed_time(b_) * 1e3 / (reps * period)
+            grown = int((self.dseq - seq0).max().item())
+            res.append(dict(first_k=k, rho=k / period, recalled=recalled, steps=reps * period, eager_us=eager_us,
+                            graph_us=graph_us, context_growth=grown))
+            log(f"[bench] decode loop first {k}/{period} Full: eager {eager_us:.1f} us/step, "
+                f"graph {graph_us:.1f} us/step, recalled {recalled}/{reps * period * B}")
+            del g
+        self.dseq.copy_(seq0)
+        return res
 
     def full_calls(self):
         P = self.P
@@ -367,6 +449,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--warm", action="store_true", help="also time back-to-back (warm) steps")
     ap.add_argument("--one-head", action="store_true", help="skip the second recall head's sweep")
+    ap.add_argument("--no-loop", action="store_true", help="skip the growing-context decode loop (graph) section")
+    ap.add_argument("--loop-only", action="store_true", help="only the decode loop section (for profiling)")
     ap.add_argument("--roofline-only", action="store_true",
                     help="only the roofline leg (always-Full calls) plus a 1 GiB copy, for PMC profiling")
     args = ap.parse_args()
@@ -380,7 +464,8 @@ def main():
     from paper_2609_20734_amd import workloads as WL
     wl = WL.ALL[args.config]
     K = args.steps
-    b = Bench(wl, args.head, args.seed, K, args.split_blocks)
+    b = Bench(wl, args.head, args.seed, K, args.split_blocks,
+              growth=0 if (args.no_loop or args.roofline_only) else 16 * 8)
     P = b.P
     local_b, gate_b, full_b = bytes_for(wl, b.seq_host, None, args.head)
     bytes_full = sum(full_b)
@@ -397,6 +482,10 @@ def main():
                           "copy_bytes": 1 << 30, "source_sha256": source_sha256()}), flush=True)
         return
 
+    if args.loop_only:
+        print(json.dumps({"decode_loop": b.decode_loop()}), flush=True)
+        return
+
     # always-Full baseline
     full = b.timed(b.full_calls(), args.warmup, cold=True)
     log(f"[bench] always-Full {full['us_mean']:.1f} us/step ({bytes_full / full['us_mean'] / 1e3:.0f} GB/s)")
@@ -410,6 +499,8 @@ def main():
         b.set_head(other)
         sweep_other = run_sweep(b, wl, args, full["us_mean"])
         b.set_head(head0)
+
+    loop = [] if args.no_loop else b.decode_loop()
 
     # roofline of the dominant kernel: the Full split-K pass over every request
     # (one launch of attn_split_kernel<128, false>; no merge launch at this size),
@@ -442,6 +533,7 @@ def main():
         "sweep": [{k: (round(v, 4) if isinstance(v, float) else v) for k, v in e.items()} for e in sweep],
         f"sweep_{other}_head": [{k: (round(v, 4) if isinstance(v, float) else v) for k, v in e.items()}
                                 for e in sweep_other],
+        "decode_loop": [{k: (round(v, 3) if isinstance(v, float) else v) for k, v in e.items()} for e in loop],
         "roofline": {k: (round(v, 4) if isinstance(v, float) else v) for k, v in roof.items()},
     }
     if not args.no_cpu_baseline:

@@ -1,8 +1,6 @@
 // Selected-state commit (App. A.5, commit equation): the chosen branch's
-// current-position K/V of every layer is appended to the paged cache in one
-// launch, then the request's length advances.  One workgroup per request:
-// it reads seq_lens[b] before any thread of it advances it, so no other
-// workgroup can observe a half-advanced length.
+// current-position K/V of every layer is appended to the paged cache, then
+// the request's length advances.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -14,7 +12,7 @@ namespace {
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBlock = 16;
-constexpr int kThreads = 256;
+constexpr int kThreads = 64;   // one wavefront: D/8 <= 16 threads work
 
 struct CommitArgs {
   uint16_t* k_cache;
@@ -31,39 +29,38 @@ struct CommitArgs {
   int32_t advance;
 };
 
-__global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
-  const int b = blockIdx.x;
-  const int n = a.seq_lens[b];
-  const int pos = n - 1;
+// One workgroup per (request, layer, KV head): thread t < D/8 moves dims
+// 8t..8t+7 of K (one 16-byte store into the [D/8][16][8] block) and of V
+// (eight 2-byte stores down the block's [D][16] column).  The lengths are
+// advanced by a second launch, so every copy reads the step's length.
+__global__ __launch_bounds__(kThreads) void commit_copy_kernel(CommitArgs a) {
+  int64_t unit = blockIdx.x;
+  const int g = (int)(unit % a.Hkv);
+  unit /= a.Hkv;
+  const int l = (int)(unit % a.L);
+  const int b = (int)(unit / a.L);
+  const int d8 = threadIdx.x;
+  if (d8 >= a.D / 8) return;
+  const int pos = a.seq_lens[b] - 1;
   const bool full = a.flags != nullptr && a.flags[b] != 0;
   const uint16_t* ks = full ? a.k_full : a.k_local;
   const uint16_t* vs = full ? a.v_full : a.v_local;
   const int64_t blk = a.block_table[(int64_t)b * a.MB + pos / kBlock];
   const int slot = pos % kBlock;
-  const int groups = a.D / 8;                       // 16-byte groups of 8 dims
-  const int64_t head_elems = (int64_t)kBlock * a.D;
-  const int64_t total = (int64_t)a.L * a.Hkv * groups;
-  for (int64_t i = threadIdx.x; i < total; i += kThreads) {
-    const int d8 = (int)(i % groups);
-    const int64_t lg = i / groups;
-    const int g = (int)(lg % a.Hkv);
-    const int l = (int)(lg / a.Hkv);
-    const int64_t src = (((int64_t)l * a.B + b) * a.Hkv + g) * a.D + d8 * 8;
-    const int64_t base = (int64_t)l * a.kv_layer_stride + (blk * a.Hkv + g) * head_elems;
-    // K block [D/8][16][8]: the 8 dims are one 16-byte group
-    *reinterpret_cast<u32x4*>(a.k_cache + base + ((int64_t)d8 * kBlock + slot) * 8) =
-        *reinterpret_cast<const u32x4*>(ks + src);
-    // V block [D][16]: dim d sits at d * 16 + slot
-    const u32x4 v = *reinterpret_cast<const u32x4*>(vs + src);
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  const int64_t src = (((int64_t)l * a.B + b) * a.Hkv + g) * a.D + d8 * 8;
+  const int64_t dst = (int64_t)l * a.kv_layer_stride + (blk * a.Hkv + g) * kBlock * a.D;
+  const u32x4 kv = *reinterpret_cast<const u32x4*>(ks + src);
+  const u32x4 vv = *reinterpret_cast<const u32x4*>(vs + src);
+  *reinterpret_cast<u32x4*>(a.k_cache + dst + ((int64_t)d8 * kBlock + slot) * 8) = kv;
+  const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const uint16_t x = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
-      a.v_cache[base + (int64_t)(d8 * 8 + e) * kBlock + slot] = x;
-    }
-  }
-  __syncthreads();
-  if (a.advance && threadIdx.x == 0) a.seq_lens[b] = n + 1;
+  for (int e = 0; e < 8; ++e)
+    a.v_cache[dst + (int64_t)(d8 * 8 + e) * kBlock + slot] = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
+}
+
+__global__ __launch_bounds__(256) void commit_advance_kernel(int32_t* seq_lens, int B) {
+  const int b = blockIdx.x * 256 + threadIdx.x;
+  if (b < B) seq_lens[b] += 1;
 }
 
 }  // namespace
@@ -104,7 +101,12 @@ extern "C" oda_status oda_commit_kv(const oda_attn_shape* shape, uint16_t* k_cac
   a.MB = shape->max_blocks_per_seq;
   a.advance = advance != 0;
   (void)hipGetLastError();
-  hipLaunchKernelGGL(commit_kernel, dim3((unsigned)shape->batch), dim3(kThreads), 0, stream, a);
+  const int64_t units = (int64_t)shape->batch * shape->num_layers * shape->num_kv_heads;
+  if (units > 0x7fffffffLL) return oda::fail(ODA_ERR_SHAPE, "grid too large");
+  hipLaunchKernelGGL(commit_copy_kernel, dim3((unsigned)units), dim3(kThreads), 0, stream, a);
+  if (a.advance)
+    hipLaunchKernelGGL(commit_advance_kernel, dim3((unsigned)oda::ceil_div(shape->batch, 256)), dim3(256), 0, stream,
+                       seq_lens, shape->batch);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return oda::fail(ODA_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return oda::ok();

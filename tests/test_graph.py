@@ -1,0 +1,88 @@
+"""Whole-step HIP graph: a period of decode steps (Local -> gate -> Full ->
+commit, per step) captured once and replayed, against the same steps run
+eagerly from the same state.  Replays are separated by eager work and host
+synchronisation, and every replay is checked (outputs of every step, the
+final caches, lengths and recall counter must be bit-identical)."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oda_synth as S
+from harness import dev_f32, dev_i32, dev_u16, need_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def test_graph_replay_matches_eager():
+    P = need_gpu()
+    L, B, Hkv, G, D, T = 2, 3, 2, 4, 128, 8
+    Hq = Hkv * G
+    s, W = 4, 24
+    seq0 = np.array([9, 40, 100], dtype=np.int32)
+    mb = int(math.ceil((seq0.max() + 4 * T) / 16))
+    table, nb = S.paged_block_table(S.rng(1, S.STREAM_TABLE), seq0 + 4 * T, mb)
+    k, v = S.kv_cache(1, L, nb, Hkv, D)
+    q = dev_u16(S.normal_bf16(S.rng(2, S.STREAM_Q), (T, L, B, Hq, D)))
+    kl, vl, kf, vf = (dev_u16(S.normal_bf16(S.rng(3 + i, S.STREAM_KCUR), (T, L, B, Hkv, D))) for i in range(4))
+    sched = np.stack([S.periodic_schedule(T, 2)] * B, axis=1).astype(np.int32)   # first 2 of every T -> Full
+    forced = dev_i32(sched)
+    d = 64
+    gate = P.gate_desc(P.HEAD_PAPER, d, 16, dev_f32(S.gate_params(4, "paper", d, 16)))
+    h, e, hl = (dev_f32(x) for x in S.gate_inputs(4, T, B, d))
+    shape = P.Shape(L, B, Hq, Hkv, D, mb, int(seq0.max()) + 4 * T, nb, 4)
+    k0, v0 = dev_u16(k), dev_u16(v)
+    dk, dv = k0.clone(), v0.clone()
+    dtab = dev_i32(table)
+    seq_init = dev_i32(seq0)
+    dseq = seq_init.clone()
+    ws_l = torch.empty(max(256, P.attn_workspace_size(shape, s, W)), dtype=torch.uint8, device="cuda")
+    ws_f = torch.empty(max(256, P.attn_workspace_size(shape, 0, 0)), dtype=torch.uint8, device="cuda")
+    ws_g = torch.empty(P.gate_workspace_size(gate, B), dtype=torch.uint8, device="cuda")
+    score = torch.empty(B, device="cuda")
+    flags = torch.empty(B, dtype=torch.int32, device="cuda")
+    wl = torch.empty(B, dtype=torch.int32, device="cuda")
+    nw = torch.empty(1, dtype=torch.int32, device="cuda")
+    ctr = torch.zeros(1, dtype=torch.int64, device="cuda")
+    outs = torch.zeros(T, L, B, Hq, D, device="cuda")
+    lses = torch.zeros(T, L, B, Hq, device="cuda")
+    scale = 1.0 / math.sqrt(D)
+
+    def period():
+        for t in range(T):
+            P.local_decode_attn(shape, P.inputs(q[t], dk, dv, dtab, dseq, scale, kl[t], vl[t]), s, W, outs[t],
+                                lses[t], ws_l)
+            P.recall_gate(gate, B, h[t], e[t], hl[t], 0.0, forced[t], score, flags, wl, nw, ctr, ws_g)
+            P.full_decode_attn(shape, P.inputs(q[t], dk, dv, dtab, dseq, scale, kf[t], vf[t]), 0, None, wl, nw,
+                               outs[t], lses[t], ws_f)
+            P.commit_kv(shape, dk, dv, dtab, dseq, kl[t], vl[t], kf[t], vf[t], flags, True)
+
+    def reset():
+        dk.copy_(k0)
+        dv.copy_(v0)
+        dseq.copy_(seq_init)
+        ctr.zero_()
+        outs.zero_()
+        lses.zero_()
+
+    reset()
+    period()                     # eager reference (also warms up every kernel)
+    torch.cuda.synchronize()
+    ref = [x.clone() for x in (outs, lses, dk, dv, dseq, ctr)]
+    assert int(ctr.item()) == 2 * B
+
+    g = torch.cuda.CUDAGraph()
+    reset()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        period()
+    for rep in range(3):
+        reset()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = (outs, lses, dk, dv, dseq, ctr)
+        for a, b_ in zip(got, ref):
+            assert torch.equal(a, b_), f"replay {rep} differs from eager"
+        _ = (outs * 2).sum().item()          # unrelated eager work between replays
