@@ -4,13 +4,19 @@
 // flagged requests.  No score is read by the host (App. A.5).
 //
 // fp32 weights and arithmetic (App. A.2).  Each dense layer is one launch of a
-// batched GEMV kernel: a wavefront owns one output row for up to 8 requests,
-// streams the row with 16-byte loads, eight 256-float chunks in flight (the
-// weights are read once per batch tile), and reduces across the wavefront.
-// (Dependent launches on one stream start back to back; a grid-wide barrier
-// inside one persistent kernel costs far more on this part.)  RMSNorm of the layer input is
+// batched GEMV kernel: an item is a group of R output rows for a tile of up to
+// 8 requests; its rows are streamed with 16-byte loads, several 256-float
+// chunks in flight, and every input load serves all R rows (the weights are
+// read once per batch tile).  Long rows split K over the four wavefronts of a
+// workgroup, which combine their sums in LDS.  RMSNorm of a layer's input is
 // folded into the same pass (the sum of squares is accumulated next to the
-// dot products), so the normalised input is never materialised.
+// dot products), so normalised inputs are never stored.
+//
+// The layers of the head are dependent launches on one stream.  A single
+// launch stepping through the layers with a barrier over its workgroups was
+// slower on this part: publishing each layer's results across the chip's L2
+// slices needs a write-back and an invalidate per workgroup per layer, which
+// costs more than a kernel boundary.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -56,114 +62,179 @@ __device__ __forceinline__ float4 absdiff4(float4 a, float4 b) {
 }
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
-template <int MODE>
+// One dense layer for a (row group, batch tile) item.  R consecutive output
+// rows share every load of the inputs (R > 1 when several requests are
+// batched, so the inputs are not re-read per row); S wavefronts of the
+// workgroup split K between them, chunk c going to wavefront c mod S (S = 4
+// for long rows, so that one launch has enough loads in flight to cover HBM
+// latency), and combine their sums through LDS.  S = 1: every wavefront of
+// the workgroup owns an item of its own.
+template <int MODE, int R, int S>
 __global__ __launch_bounds__(256) void gate_linear_kernel(LinArgs p) {
   constexpr bool kNorm = (MODE == kTower || MODE == kGateUp);
   constexpr bool kTwo = (MODE == kGateUp);
+  constexpr int kAcc = R * kBatchTile;
+  static_assert(S == 1 || S == kWaves, "K is split over all wavefronts or none");
+  __shared__ float sm[S > 1 ? kWaves : 1][S > 1 ? (kTwo ? 2 : 1) * kAcc + kBatchTile : 1];
   const int lane = threadIdx.x & 63;
   const int wave = uniform(threadIdx.x >> 6);
-  const int gw = blockIdx.x * kWaves + wave;
-  const int row0 = gw % p.rows;           // one output row per wavefront
-  const int b0 = (gw / p.rows) * kBatchTile;
-  if (b0 >= p.B) return;
+  const int item = S == 1 ? blockIdx.x * kWaves + wave : blockIdx.x;
+  const int part = S == 1 ? 0 : wave;
+  const int groups = p.rows / R;             // the host keeps rows (and dt) multiples of R
+  const int rg = item % groups;
+  const int b0 = (item / groups) * kBatchTile;
+  if (b0 >= p.B) return;                     // uniform over the workgroup when S > 1
   const int nb = min(kBatchTile, p.B - b0);
 
   const float* W = p.W;
   const float* bias = p.bias;
   const float* gain = p.gain;
   const float* X = p.X[0];
-  int tower = 0, row = row0;
-  if (MODE == kTower) {
+  int tower = 0, row0 = rg * R;
+  if (MODE == kTower) {                      // dt % R == 0: a group never straddles two towers
     tower = row0 / p.dt;
-    row = row0 - tower * p.dt;
+    row0 -= tower * p.dt;
     W += tower * p.w_stride;
     bias += tower * p.w_stride;
     gain += tower * p.w_stride;
     X = p.X[tower];
   }
-  const float* wrow = W + (int64_t)row * p.K;
-  const float* wrow2 = kTwo ? p.W2 + (int64_t)row * p.K : nullptr;
+  const float* wrow = W + (int64_t)row0 * p.K;
+  const float* wrow2 = kTwo ? p.W2 + (int64_t)row0 * p.K : nullptr;
 
-  float acc[kBatchTile], acc2[kBatchTile], ss[kBatchTile];
+  float acc[R][kBatchTile], acc2[kTwo ? R : 1][kBatchTile], ss[kBatchTile];
 #pragma unroll
-  for (int bi = 0; bi < kBatchTile; ++bi) acc[bi] = acc2[bi] = ss[bi] = 0.f;
+  for (int bi = 0; bi < kBatchTile; ++bi) {
+    ss[bi] = 0.f;
+#pragma unroll
+    for (int j = 0; j < R; ++j) acc[j][bi] = 0.f;
+#pragma unroll
+    for (int j = 0; j < (kTwo ? R : 1); ++j) acc2[j][bi] = 0.f;
+  }
 
   auto step = [&](int k) {
-    const float4 w = *reinterpret_cast<const float4*>(wrow + k);
-    float4 w2 = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (kTwo) w2 = *reinterpret_cast<const float4*>(wrow2 + k);
+    float4 w[R], w2[kTwo ? R : 1];
+#pragma unroll
+    for (int j = 0; j < R; ++j) w[j] = *reinterpret_cast<const float4*>(wrow + (int64_t)j * p.K + k);
+    if (kTwo) {
+#pragma unroll
+      for (int j = 0; j < R; ++j) w2[j] = *reinterpret_cast<const float4*>(wrow2 + (int64_t)j * p.K + k);
+    }
     float4 gk = make_float4(1.f, 1.f, 1.f, 1.f);
     if (kNorm) gk = *reinterpret_cast<const float4*>(gain + k);
 #pragma unroll
     for (int bi = 0; bi < kBatchTile; ++bi) {
       if (bi < nb) {
-        const int b = b0 + bi;
-        const float4 x = *reinterpret_cast<const float4*>(X + (int64_t)b * p.K + k);
+        const float4 x = *reinterpret_cast<const float4*>(X + (int64_t)(b0 + bi) * p.K + k);
         if (kNorm) ss[bi] += dot4(x, x);
         const float4 xg = kNorm ? mul4(x, gk) : x;
-        acc[bi] += dot4(w, xg);
-        if (kTwo) acc2[bi] += dot4(w2, xg);
+#pragma unroll
+        for (int j = 0; j < R; ++j) {
+          acc[j][bi] += dot4(w[j], xg);
+          if (kTwo) acc2[j][bi] += dot4(w2[j], xg);
+        }
       }
     }
   };
-  // whole 256-float chunks (every lane busy), unrolled so their loads overlap
+  // this wavefront's whole 256-float chunks (every lane busy), unrolled so
+  // their loads overlap, then the ragged tail chunk if it is ours
   const int full = p.K / 256;
-#pragma unroll 8
-  for (int c = 0; c < full; ++c) step(c * 256 + 4 * lane);
-  if (full * 256 + 4 * lane < p.K) step(full * 256 + 4 * lane);
+  const int mine_full = full > part ? (full - part + S - 1) / S : 0;
+  constexpr int kUnroll = R == 1 ? 8 : 4;
+#pragma unroll kUnroll
+  for (int i = 0; i < mine_full; ++i) step((part + i * S) * 256 + 4 * lane);
+  if (full % S == part && full * 256 + 4 * lane < p.K) step(full * 256 + 4 * lane);
 
-  // reduce; lane bi finishes request b0 + bi
-  float mine = 0.f, mine2 = 0.f, my_ss = 0.f;
+  // reduce over the wavefront; lane j * 8 + bi keeps row j, request bi
+  float v = 0.f, v2 = 0.f, my_ss = 0.f;
 #pragma unroll
   for (int bi = 0; bi < kBatchTile; ++bi) {
     if (bi < nb) {
       const float s = kNorm ? wave_sum(ss[bi]) : 0.f;
-      const float v = wave_sum(acc[bi]);
-      const float v2 = kTwo ? wave_sum(acc2[bi]) : 0.f;
-      if (lane == bi) {
-        mine = v;
-        mine2 = v2;
-        my_ss = s;
+      if (kNorm && lane == bi) my_ss = s;
+#pragma unroll
+      for (int j = 0; j < R; ++j) {
+        const float t = wave_sum(acc[j][bi]);
+        const float t2 = kTwo ? wave_sum(acc2[j][bi]) : 0.f;
+        if (lane == j * kBatchTile + bi) {
+          v = t;
+          v2 = t2;
+        }
       }
     }
   }
-  if (lane >= nb) return;
-  const int b = b0 + lane;
+  if (S > 1) {   // combine the K parts: wave w's sums go to sm[w], wave 0 adds them in order
+    if (lane < kAcc) {
+      sm[wave][lane] = v;
+      if (kTwo) sm[wave][kAcc + lane] = v2;
+    }
+    if (kNorm && lane < kBatchTile) sm[wave][(kTwo ? 2 : 1) * kAcc + lane] = my_ss;
+    __syncthreads();
+    if (wave != 0) return;
+    if (lane < kAcc) {
+      v = sm[0][lane];
+      v2 = kTwo ? sm[0][kAcc + lane] : 0.f;
+#pragma unroll
+      for (int w = 1; w < S; ++w) {
+        v += sm[w][lane];
+        if (kTwo) v2 += sm[w][kAcc + lane];
+      }
+    }
+    if (kNorm) {
+      const int bi = lane % kBatchTile;
+      my_ss = sm[0][(kTwo ? 2 : 1) * kAcc + bi];
+#pragma unroll
+      for (int w = 1; w < S; ++w) my_ss += sm[w][(kTwo ? 2 : 1) * kAcc + bi];
+    }
+  } else if (kNorm) {
+    my_ss = __shfl(my_ss, lane % kBatchTile);   // lane j * 8 + bi needs request bi's sum of squares
+  }
+  const int j = lane / kBatchTile, bi = lane % kBatchTile;
+  if (lane >= kAcc || bi >= nb) return;
+  const int b = b0 + bi;
+  const int row = row0 + j;
   const float inv = kNorm ? rsqrtf(my_ss / (float)p.K + p.eps) : 1.f;
   if (MODE == kTower) {
-    p.Y[((int64_t)tower * p.B + b) * p.dt + row] = silu(mine * inv + bias[row]);
+    p.Y[((int64_t)tower * p.B + b) * p.dt + row] = silu(v * inv + bias[row]);
   } else if (MODE == kMlpHidden) {
-    p.Y[(int64_t)b * p.rows + row] = gelu(mine + bias[row]);
+    p.Y[(int64_t)b * p.rows + row] = gelu(v + bias[row]);
   } else if (MODE == kGateUp) {
-    p.Y[(int64_t)b * p.rows + row] = silu(mine * inv) * (mine2 * inv);
+    p.Y[(int64_t)b * p.rows + row] = silu(v * inv) * (v2 * inv);
   } else {  // kDown
-    p.Y[(int64_t)b * p.rows + row] = p.aux[(int64_t)b * p.rows + row] + mine;
+    p.Y[(int64_t)b * p.rows + row] = p.aux[(int64_t)b * p.rows + row] + v;
   }
 }
 
 // Fusion layer of App. A.2: z0 = (a + b + c + SiLU(W_f u + b_f)) / 2 with the
-// interaction vector u = [a; b; c; a*b; |a-b|; a*c; |a-c|; b*c; |b-c|].  One
-// wavefront per (output row, batch tile); lanes walk the tower index m four at
-// a time and build the nine parts of u for those m in registers, so u is never
+// interaction vector u = [a; b; c; a*b; |a-b|; a*c; |a-c|; b*c; |b-c|].  Item:
+// one output row for a batch tile.  Lanes walk the tower index m four at a
+// time and build the nine parts of u for those m in registers, so u is never
 // stored and W_f's nine column blocks are read with coalesced 16-byte loads.
+// S wavefronts share an item, taking alternate 256-wide steps of m, and add
+// their sums through LDS (S > 1 for wide towers, so that the launch has
+// enough wavefronts in flight).
+template <int S>
 __global__ __launch_bounds__(256) void gate_fusion_kernel(LinArgs p) {
+  static_assert(kWaves % S == 0, "items per workgroup");
+  __shared__ float sm[S > 1 ? kWaves : 1][kBatchTile];
   const int lane = threadIdx.x & 63;
   const int wave = uniform(threadIdx.x >> 6);
-  const int gw = blockIdx.x * kWaves + wave;
-  const int row = gw % p.rows;
-  const int b0 = (gw / p.rows) * kBatchTile;
-  if (b0 >= p.B) return;
-  const int nb = min(kBatchTile, p.B - b0);
+  const int part = wave % S;
+  const int item = blockIdx.x * (kWaves / S) + wave / S;
+  const int row = item % p.rows;
+  const int b0 = (item / p.rows) * kBatchTile;
+  const bool valid = b0 < p.B;
+  const int nb = valid ? min(kBatchTile, p.B - b0) : 0;
   const int dt = p.dt;
   const float* wrow = p.W + (int64_t)row * 9 * dt;
   const float* abc = p.aux;
   float acc[kBatchTile];
 #pragma unroll
   for (int bi = 0; bi < kBatchTile; ++bi) acc[bi] = 0.f;
-  for (int m = 4 * lane; m < dt; m += 256) {
+  for (int m = (part * 64 + lane) * 4; valid && m < dt; m += 256 * S) {
     float4 w[9];
 #pragma unroll
-    for (int part = 0; part < 9; ++part) w[part] = *reinterpret_cast<const float4*>(wrow + part * dt + m);
+    for (int q = 0; q < 9; ++q) w[q] = *reinterpret_cast<const float4*>(wrow + q * dt + m);
 #pragma unroll
     for (int bi = 0; bi < kBatchTile; ++bi) {
       if (bi < nb) {
@@ -183,6 +254,15 @@ __global__ __launch_bounds__(256) void gate_fusion_kernel(LinArgs p) {
     if (bi < nb) {
       const float v = wave_sum(acc[bi]);
       if (lane == bi) mine = v;
+    }
+  }
+  if (S > 1) {   // the item's S partial sums, added in order by its first wavefront
+    if (lane < kBatchTile) sm[wave][lane] = mine;
+    __syncthreads();
+    if (part != 0) return;
+    if (lane < kBatchTile) {
+#pragma unroll
+      for (int q = 1; q < S; ++q) mine += sm[wave + q][lane];
     }
   }
   if (lane >= nb) return;
@@ -207,16 +287,21 @@ struct FinalArgs {
   float eps, tau;
 };
 
-// One wavefront: the scalar projection for every request, then the decision
-// and the ascending compaction (ballot + prefix popcount).
-__global__ __launch_bounds__(64) void gate_final_kernel(FinalArgs p) {
-  const int lane = threadIdx.x;
+constexpr int kFinalWaves = 16;
+
+// The scalar projection q = w . RMSNorm(x) + b (w . x + b without a gain) for
+// every request, spread over the workgroup's wavefronts 64 requests at a
+// time, then the decision and the ascending compaction of the flagged
+// requests (ballot + prefix popcount) by wavefront 0.
+__global__ __launch_bounds__(kFinalWaves * 64) void gate_final_kernel(FinalArgs p) {
+  __shared__ float sm_score[64];
+  const int lane = threadIdx.x & 63;
+  const int wave = uniform(threadIdx.x >> 6);
   const bool norm = p.gain != nullptr;
   int total = 0;
   for (int c0 = 0; c0 < p.B; c0 += 64) {
-    float my_score = 0.f;
     const int nc = min(64, p.B - c0);
-    for (int i = 0; i < nc; ++i) {
+    for (int i = wave; i < nc; i += kFinalWaves) {
       const int b = c0 + i;
       float dot = 0.f, ss = 0.f;
       for (int k = 4 * lane; k < p.K; k += 256) {
@@ -231,25 +316,29 @@ __global__ __launch_bounds__(64) void gate_final_kernel(FinalArgs p) {
       dot = wave_sum(dot);
       float s = dot;
       if (norm) s = dot * rsqrtf(wave_sum(ss) / (float)p.K + p.eps);
-      s += p.bias[0];
-      if (lane == i) my_score = s;
+      if (lane == 0) sm_score[i] = s + p.bias[0];
     }
-    const int b = c0 + lane;
-    bool flag = false;
-    if (lane < nc) {
-      p.score[b] = my_score;
-      flag = p.forced ? (p.forced[b] != 0) : (my_score > p.tau);
-      flag = flag || !__builtin_isfinite(my_score);
-      p.flags[b] = flag ? 1 : 0;
+    __syncthreads();
+    if (wave == 0) {
+      const int b = c0 + lane;
+      bool flag = false;
+      if (lane < nc) {
+        const float s = sm_score[lane];
+        p.score[b] = s;
+        flag = p.forced ? (p.forced[b] != 0) : (s > p.tau);
+        flag = flag || !__builtin_isfinite(s);
+        p.flags[b] = flag ? 1 : 0;
+      }
+      const uint64_t mask = __ballot(flag);
+      if (flag && p.work_list) {
+        const uint64_t below = lane ? (mask & ((~0ull) >> (64 - lane))) : 0ull;
+        p.work_list[total + __popcll(below)] = b;
+      }
+      total += __popcll(mask);
     }
-    const uint64_t mask = __ballot(flag);
-    if (flag && p.work_list) {
-      const uint64_t below = lane ? (mask & ((~0ull) >> (64 - lane))) : 0ull;
-      p.work_list[total + __popcll(below)] = b;
-    }
-    total += __popcll(mask);
+    __syncthreads();
   }
-  if (lane == 0) {
+  if (threadIdx.x == 0) {
     if (p.n_work) p.n_work[0] = total;
     // integer add at the memory side: no round trip before the kernel can retire
     if (p.counter) atomicAdd(reinterpret_cast<unsigned long long*>(p.counter), (unsigned long long)total);
@@ -323,11 +412,52 @@ oda_status check_gate(const oda_gate_desc* g) {
   return ODA_OK;
 }
 
+template <int MODE, int R, int S>
+void launch_linear_rs(const LinArgs& a, hipStream_t stream) {
+  const int64_t items = (int64_t)(a.rows / R) * oda::ceil_div(a.B, kBatchTile);
+  const int64_t groups = S == 1 ? oda::ceil_div(items, kWaves) : items;
+  hipLaunchKernelGGL((gate_linear_kernel<MODE, R, S>), dim3((unsigned)groups), dim3(256), 0, stream, a);
+}
+
+// Launch shape of a dense layer.  K is split over the four wavefronts of a
+// workgroup when rows are long (K >= 4096), or when there are too few items
+// to occupy the chip (< 1024) and every wavefront still gets whole chunks.
+// With more than two requests per tile, R = 4 (else 2) rows share each input
+// load while that still leaves >= 512 workgroups.
 template <int MODE>
 void launch_linear(const LinArgs& a, hipStream_t stream) {
-  const int waves = a.rows * (int)oda::ceil_div(a.B, kBatchTile);
-  hipLaunchKernelGGL(gate_linear_kernel<MODE>, dim3((unsigned)oda::ceil_div(waves, kWaves)), dim3(256), 0,
-                     stream, a);
+  const int tiles = (int)oda::ceil_div(a.B, kBatchTile);
+  const int per_tile = std::min(a.B, kBatchTile);
+  const int unit = MODE == kTower ? a.dt : a.rows;   // R must divide it
+  const int64_t items = (int64_t)a.rows * tiles;
+  const bool split = a.K >= 4096 || (a.K >= 1024 && items < 1024);
+  auto fits = [&](int r) {
+    return per_tile > 2 && unit % r == 0 && items / r / (split ? 1 : kWaves) >= 512;
+  };
+  if (split) {
+    if (fits(4)) return launch_linear_rs<MODE, 4, kWaves>(a, stream);
+    if (fits(2)) return launch_linear_rs<MODE, 2, kWaves>(a, stream);
+    return launch_linear_rs<MODE, 1, kWaves>(a, stream);
+  }
+  if (fits(4)) return launch_linear_rs<MODE, 4, 1>(a, stream);
+  if (fits(2)) return launch_linear_rs<MODE, 2, 1>(a, stream);
+  launch_linear_rs<MODE, 1, 1>(a, stream);
+}
+
+// Fusion launch: S wavefronts per item when the tower width allows S steps
+// of 256 and the items alone would leave the chip under-occupied.
+void launch_fusion(const LinArgs& a, hipStream_t stream) {
+  const int64_t items = (int64_t)a.rows * oda::ceil_div(a.B, kBatchTile);
+  const int steps = (int)oda::ceil_div(a.dt, 256);
+  const int s = items >= 2048 ? 1 : steps >= 4 ? 4 : steps >= 2 ? 2 : 1;
+  const unsigned groups = (unsigned)oda::ceil_div(items * s, kWaves);
+  if (s == 4) {
+    hipLaunchKernelGGL(gate_fusion_kernel<4>, dim3(groups), dim3(256), 0, stream, a);
+  } else if (s == 2) {
+    hipLaunchKernelGGL(gate_fusion_kernel<2>, dim3(groups), dim3(256), 0, stream, a);
+  } else {
+    hipLaunchKernelGGL(gate_fusion_kernel<1>, dim3(groups), dim3(256), 0, stream, a);
+  }
 }
 
 }  // namespace
@@ -424,10 +554,7 @@ extern "C" oda_status oda_recall_gate(const oda_gate_desc* gate, int32_t batch, 
     a.Y = z0;
     a.rows = dt;
     a.K = 9 * dt;
-    {
-      const int waves = a.rows * (int)oda::ceil_div(a.B, kBatchTile);
-      hipLaunchKernelGGL(gate_fusion_kernel, dim3((unsigned)oda::ceil_div(waves, kWaves)), dim3(256), 0, stream, a);
-    }
+    launch_fusion(a, stream);
     // two pre-RMSNorm residual SwiGLU blocks
     float* zin = z0;
     float* zout = z1;
@@ -481,7 +608,9 @@ extern "C" oda_status oda_recall_gate(const oda_gate_desc* gate, int32_t batch, 
     fa.bias = P + (int64_t)dt * d + 2 * dt;
     fa.K = dt;
   }
-  hipLaunchKernelGGL(gate_final_kernel, dim3(1), dim3(64), 0, stream, fa);
+  // one wavefront per request in flight, at most kFinalWaves
+  const int final_threads = 64 * std::min(kFinalWaves, batch);
+  hipLaunchKernelGGL(gate_final_kernel, dim3(1), dim3((unsigned)final_threads), 0, stream, fa);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return oda::fail(ODA_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return oda::ok();

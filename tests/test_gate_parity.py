@@ -64,7 +64,11 @@ def _check(g, h, e, l, tau, forced=None):
 
 @pytest.mark.parametrize("kind,d,dh,B", [("mlp", 512, 64, 1), ("mlp", 512, 64, 13), ("paper", 512, 64, 1),
                                          ("paper", 64, 16, 9), ("paper", 4096, 256, 1), ("mlp", 4096, 256, 32),
-                                         ("paper", 4096, 256, 32), ("paper", 8192, 512, 8)])
+                                         ("paper", 4096, 256, 32), ("paper", 8192, 512, 8),
+                                         # launch shapes: K split over a workgroup, grouped rows, ragged
+                                         # tiles and chunk tails, wide towers, batches over 64
+                                         ("paper", 2048, 1024, 1), ("paper", 4096, 260, 70),
+                                         ("paper", 256, 516, 2), ("mlp", 8192, 512, 8), ("mlp", 4096, 256, 70)])
 def test_scores_and_flags(kind, d, dh, B):
     g = Gate(kind, d, dh, B)
     h, e, l = (x[0] for x in S.gate_inputs(3, 1, B, d))
