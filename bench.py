@@ -296,6 +296,26 @@ class Bench:
                     us_max=float(per.max()), bracket_us=float(t_all0.elapsed_time(t_all1) * 1e3 / K),
                     wall_us=wall * 1e6 / K, per_step=per, recalled=int(self.counter.item()))
 
+    def local_layout(self, reps=20):
+        """Local attention alone (every stack, cold) reading the window through
+        the permuted block table and through a contiguous one (identity table,
+        same cache, same lengths): the cost of scattered paged-window reads,
+        which decides whether a contiguous ring workspace for Local would pay."""
+        import oda_synth as S
+        torch, P = self.torch, self.P
+        seq = self.seq_host + self.growth
+        mb = self.stacks[0].shape.max_blocks_per_seq
+        ident, nb = S.paged_block_table(S.rng(self.seed, S.STREAM_TABLE), seq, mb, permute=False)
+        assert nb == self.stacks[0].shape.num_blocks
+        dident = torch.from_numpy(ident).to(self.dev)
+        scale = 1.0 / math.sqrt(self.wl.head_dim)
+        res = {}
+        for name, table in (("permuted", self.dtable), ("contiguous", dident)):
+            calls = [P.prepare_local(st.shape, P.inputs(st.q, st.k, st.v, table, self.dseq, scale), *st.local_args,
+                                     st.out, st.lse, st.ws_local) for st in self.stacks]
+            res[f"{name}_us"] = self.kernel_time(calls, reps, cold=True)
+        return res
+
     def kernel_time(self, calls, reps, cold=True):
         """Mean duration (us) of one call bracketed by events on its stream."""
         torch = self.torch
@@ -501,6 +521,9 @@ def main():
         b.set_head(head0)
 
     loop = [] if args.no_loop else b.decode_loop()
+    layout = b.local_layout()
+    log(f"[bench] Local alone, cold: permuted block table {layout['permuted_us']:.1f} us, "
+        f"contiguous table {layout['contiguous_us']:.1f} us")
 
     # roofline of the dominant kernel: the Full split-K pass over every request
     # (one launch of attn_split_kernel<128, false>; no merge launch at this size),
@@ -534,6 +557,7 @@ def main():
         f"sweep_{other}_head": [{k: (round(v, 4) if isinstance(v, float) else v) for k, v in e.items()}
                                 for e in sweep_other],
         "decode_loop": [{k: (round(v, 3) if isinstance(v, float) else v) for k, v in e.items()} for e in loop],
+        "local_window_layout": {k: round(v, 3) for k, v in layout.items()},
         "roofline": {k: (round(v, 4) if isinstance(v, float) else v) for k, v in roof.items()},
     }
     if not args.no_cpu_baseline:
