@@ -214,6 +214,75 @@ oda_status oda_commit_kv(const oda_attn_shape *shape, uint16_t *k_cache, uint16_
                          const uint16_t *v_local, const uint16_t *k_full, const uint16_t *v_full,
                          const int32_t *flags, int32_t advance, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * The decoder around the hot path (the backbone f_theta of §2.1 that Local and
+ * Full share; App. A.6's cost model).  A pre-norm decoder layer is, per request:
+ *   qkv = W_qkv . RMSNorm(h)              oda_dense_bf16 (gain = input norm)
+ *   q, k, v = split(qkv); q, k per-head RMSNorm and rotary embedding at the
+ *   current position, cast to bf16       oda_qk_norm_rope
+ *   a = attention(q, cache, k, v)         oda_local_decode_attn / oda_full_decode_attn
+ *   h = h + W_o . a                       oda_dense_bf16 (residual = h)
+ *   m = SiLU(W_g . RMSNorm(h)) * (W_u . RMSNorm(h))   oda_dense_bf16 (SWIGLU)
+ *   h = h + W_d . m                       oda_dense_bf16 (residual = h)
+ * then logits = W_vocab . RMSNorm(h) and the greedy token (oda_argmax).
+ * Weights bf16, activations fp32.  Every call below can be restricted to the
+ * recall gate's list (work_list, n_work: both NULL = every request; entries
+ * must be in [0, batch)): only those requests are read and written.
+ * ------------------------------------------------------------------------- */
+
+typedef enum { ODA_DENSE_PLAIN = 0, ODA_DENSE_SWIGLU = 1 } oda_dense_mode;
+
+typedef struct {
+  int32_t in_features;     /* K, a multiple of 8                                  */
+  int32_t out_features;    /* N                                                   */
+  int32_t mode;            /* oda_dense_mode                                      */
+  float rms_eps;           /* RMSNorm epsilon (used when norm_gain != NULL)       */
+  const uint16_t *weight;  /* device bf16, PLAIN: [N][K]; SWIGLU: [2N][K], the N
+                              gate rows then the N up rows; 16-byte aligned       */
+  const float *norm_gain;  /* device fp32 [K]: x' = x / sqrt(mean(x^2) + eps) * gain;
+                              NULL: x' = x                                        */
+} oda_dense_desc;
+
+/* Dense layer for `batch` requests, fp32 accumulation:
+ *   PLAIN:  y[b][r] = sum_k W[r][k] x'[b][k]  (+ residual[b][r] if residual != NULL)
+ *   SWIGLU: y[b][r] = SiLU(sum_k W[r][k] x'[b][k]) * sum_k W[N + r][k] x'[b][k]
+ *           (no residual)
+ * x fp32 [batch][K] (16-byte aligned); residual, y fp32 [batch][N].  y may be
+ * the residual buffer (in-place residual add); x must not overlap y. */
+oda_status oda_dense_bf16(const oda_dense_desc *desc, int32_t batch, const float *x, const float *residual,
+                          float *y, const int32_t *work_list, const int32_t *n_work, hipStream_t stream);
+
+/* Query/key preparation for the current token.  qkv fp32 [batch][(Hq + 2 Hkv) D]
+ * holds the q heads, then the k heads, then the v heads.  q and k heads get a
+ * per-head RMSNorm (gains q_gain / k_gain fp32 [D], or NULL for none) and then
+ * the rotary embedding at position p = seq_lens[b] - 1 (rotate-half pairing:
+ * dims i and i + D/2 rotate by angle p * theta^(-2i/D), angles in double);
+ * results are rounded to bf16 (nearest-even):
+ *   q_out bf16 [batch][Hq][D] (the attention query; as q of a one-layer call),
+ *   k_out, v_out bf16 [batch][Hkv][D] (the current candidate, k_cur / v_cur).
+ * D even, at most 128. */
+oda_status oda_qk_norm_rope(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                            const float *qkv, const float *q_gain, const float *k_gain, float rms_eps,
+                            double rope_theta, const int32_t *seq_lens, uint16_t *q_out, uint16_t *k_out,
+                            uint16_t *v_out, const int32_t *work_list, const int32_t *n_work,
+                            hipStream_t stream);
+
+/* x[b] = table[tokens[b]] widened to fp32; table bf16 [vocab][d_model] (d_model a
+ * multiple of 8); a token outside [0, vocab) gives a NaN row (and so a nonfinite
+ * recall score, i.e. Full). */
+oda_status oda_embed_bf16(const uint16_t *table, int32_t vocab, int32_t d_model, int32_t batch,
+                          const int32_t *tokens, float *x, hipStream_t stream);
+
+/* dst[b] = src[b] (fp32 rows of row_len, a multiple of 4) for the listed
+ * requests (all if the list is NULL): moves the Full retry's results into the
+ * selected state. */
+oda_status oda_copy_rows(int32_t batch, int32_t row_len, const float *src, float *dst,
+                         const int32_t *work_list, const int32_t *n_work, hipStream_t stream);
+
+/* index[b] = the first position of the largest non-NaN value of x[b][0..n)
+ * (-1 if all are NaN); x fp32 [batch][n], n a multiple of 4. */
+oda_status oda_argmax(int32_t batch, int32_t n, const float *x, int32_t *index, hipStream_t stream);
+
 /* Static description of a status code. */
 const char *oda_status_string(oda_status status);
 

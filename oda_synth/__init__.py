@@ -37,6 +37,8 @@ STREAM_GATE_PARAMS = 7
 STREAM_GATE_INPUTS = 8
 STREAM_SEQ_LENS = 9
 STREAM_FORCED = 10
+STREAM_DECODER = 11
+STREAM_TOKENS = 12
 
 
 def rng(seed: int, stream: int) -> np.random.Generator:
@@ -61,9 +63,12 @@ def bf16_bits_to_f32(bits) -> np.ndarray:
     return b.view(np.float32)
 
 
-def normal_bf16(g: np.random.Generator, shape) -> np.ndarray:
-    """N(0,1) samples rounded to bf16, as raw uint16 bits."""
-    return f32_to_bf16_bits(g.standard_normal(size=shape, dtype=np.float32))
+def normal_bf16(g: np.random.Generator, shape, std: float = 1.0) -> np.ndarray:
+    """N(0, std^2) samples rounded to bf16, as raw uint16 bits."""
+    x = g.standard_normal(size=shape, dtype=np.float32)
+    if std != 1.0:
+        x = (x * np.float32(std)).astype(np.float32)
+    return f32_to_bf16_bits(x)
 
 
 def paged_block_table(g: np.random.Generator, seq_lens, max_blocks_per_seq: int | None = None,
@@ -168,8 +173,8 @@ def periodic_schedule(steps: int, first_k: int, period: int = 16) -> np.ndarray:
 # device fill for caches too large to build on the host
 # --------------------------------------------------------------------------
 
-def fill_normal_bf16_(t, seed: int, stream: int, chunk_elems: int = 1 << 28) -> None:
-    """Fill a CUDA tensor (dtype bfloat16 or int16 view of one) with N(0,1)
+def fill_normal_bf16_(t, seed: int, stream: int, chunk_elems: int = 1 << 28, std: float = 1.0) -> None:
+    """Fill a CUDA tensor (dtype bfloat16 or int16 view of one) with N(0, std^2)
     bf16 values drawn from torch's Philox generator, in chunks."""
     import torch
     g = torch.Generator(device=t.device)
@@ -180,4 +185,61 @@ def fill_normal_bf16_(t, seed: int, stream: int, chunk_elems: int = 1 << 28) -> 
     n = flat.numel()
     for s in range(0, n, chunk_elems):
         e = min(n, s + chunk_elems)
-        flat[s:e].normal_(0.0, 1.0, generator=g)
+        flat[s:e].normal_(0.0, float(std), generator=g)
+
+
+# ---------------------------------------------------------------------------
+# the decoder around the hot path (synthetic weights of a given shape)
+# ---------------------------------------------------------------------------
+
+def decoder_tensor_specs(L: int, d: int, Hq: int, Hkv: int, D: int, F: int, V: int):
+    """(name, shape, kind, std) of every decoder tensor.  kind "w": bf16 weight
+    ~ N(0, std^2); "g": fp32 RMSNorm gain 1 + 0.02 N(0,1).  Dense weights are
+    [out][in]; w_gu holds the F gate rows then the F up rows; the vocabulary
+    projection is the embedding table (tied)."""
+    qkv = (Hq + 2 * Hkv) * D
+    return [("embed", (V, d), "w", 1.0),
+            ("attn_norm", (L, d), "g", 0.0),
+            ("w_qkv", (L, qkv, d), "w", d ** -0.5),
+            ("q_norm", (L, D), "g", 0.0),
+            ("k_norm", (L, D), "g", 0.0),
+            ("w_o", (L, d, Hq * D), "w", (Hq * D) ** -0.5),
+            ("mlp_norm", (L, d), "g", 0.0),
+            ("w_gu", (L, 2 * F, d), "w", d ** -0.5),
+            ("w_down", (L, d, F), "w", F ** -0.5),
+            ("final_norm", (d,), "g", 0.0)]
+
+
+def decoder_weights(seed: int, L: int, d: int, Hq: int, Hkv: int, D: int, F: int, V: int) -> dict:
+    """Host arrays (bf16 bits as uint16, gains as float32) for small shapes."""
+    g = rng(seed, STREAM_DECODER)
+    out = {}
+    for name, shape, kind, std in decoder_tensor_specs(L, d, Hq, Hkv, D, F, V):
+        if kind == "w":
+            out[name] = normal_bf16(g, shape, std)
+        else:
+            out[name] = (1.0 + 0.02 * g.standard_normal(shape)).astype(np.float32)
+    return out
+
+
+def decoder_weights_device(seed: int, L: int, d: int, Hq: int, Hkv: int, D: int, F: int, V: int, device) -> dict:
+    """Device tensors of the same tensors, filled with torch's Philox generator
+    (full-size models; not the same values as decoder_weights)."""
+    import torch
+    out = {}
+    for i, (name, shape, kind, std) in enumerate(decoder_tensor_specs(L, d, Hq, Hkv, D, F, V)):
+        if kind == "w":
+            t = torch.empty(shape, dtype=torch.bfloat16, device=device)
+            fill_normal_bf16_(t, seed, STREAM_DECODER * 100 + i, std=std)
+        else:
+            t = torch.empty(shape, dtype=torch.float32, device=device)
+            gen = torch.Generator(device=device)
+            gen.manual_seed(int(seed) * 1000003 + STREAM_DECODER * 100 + i)
+            t.normal_(0.0, 0.02, generator=gen).add_(1.0)
+        out[name] = t
+    return out
+
+
+def tokens(seed: int, steps: int, batch: int, vocab: int) -> np.ndarray:
+    """A fixed continuation: uniform token ids, int32 [steps][B]."""
+    return rng(seed, STREAM_TOKENS).integers(0, vocab, size=(steps, batch)).astype(np.int32)

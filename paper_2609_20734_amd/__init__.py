@@ -2,7 +2,9 @@
 
 The product is the C-ABI library ``liboda.so`` (include/oda.h): hand-written
 HIP kernels for Local decode attention, the recall gate with its device
-predicate, and Full decode attention for flagged requests only.  This package
+predicate, Full decode attention for flagged requests only, the selected-state
+commit, and the decoder layers around them (``decoder`` composes a whole
+synthetic decode step from those entry points).  This package
 holds its sources (``csrc/``), its build step (``build.py``), a ctypes
 binding with the same entry-point names (``_lib``), the byte accounting used
 to report bandwidth (``ledger``) and the synthetic workload shapes
@@ -13,7 +15,10 @@ not been built that raises ImportError (there is no fallback path).
 """
 _EXPORTS = ("HEAD_MLP", "HEAD_PAPER", "OdaError", "Shape", "attn_workspace_size", "full_decode_attn",
             "gate_desc", "gate_param_count", "gate_workspace_size", "inputs", "local_decode_attn",
-            "recall_gate", "lib", "prepare_local", "prepare_full", "prepare_gate", "Call", "commit_kv", "prepare_commit")
+            "recall_gate", "lib", "prepare_local", "prepare_full", "prepare_gate", "Call", "commit_kv", "prepare_commit",
+            "DENSE_PLAIN", "DENSE_SWIGLU", "dense_desc", "dense_bf16", "qk_norm_rope", "embed_bf16", "copy_rows",
+            "argmax", "prepare_dense", "prepare_qk_norm_rope", "prepare_embed", "prepare_copy_rows",
+            "prepare_argmax")
 
 
 def __getattr__(name):

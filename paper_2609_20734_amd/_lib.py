@@ -30,8 +30,12 @@ ODA_ERR_HIP = -5
 HEAD_PAPER = 0
 HEAD_MLP = 1
 
+DENSE_PLAIN = 0
+DENSE_SWIGLU = 1
+
 EXPORTED = ("oda_attn_workspace_size", "oda_local_decode_attn", "oda_full_decode_attn",
             "oda_gate_param_count", "oda_gate_workspace_size", "oda_recall_gate", "oda_commit_kv",
+            "oda_dense_bf16", "oda_qk_norm_rope", "oda_embed_bf16", "oda_copy_rows", "oda_argmax",
             "oda_status_string", "oda_last_error")
 
 
@@ -62,7 +66,13 @@ class GateDesc(ctypes.Structure):
                 ("rms_eps", ctypes.c_float), ("params", ctypes.c_void_p)]
 
 
+class DenseDesc(ctypes.Structure):
+    _fields_ = [("in_features", ctypes.c_int32), ("out_features", ctypes.c_int32), ("mode", ctypes.c_int32),
+                ("rms_eps", ctypes.c_float), ("weight", ctypes.c_void_p), ("norm_gain", ctypes.c_void_p)]
+
+
 _P = ctypes.POINTER
+_V = ctypes.c_void_p
 _lib.oda_attn_workspace_size.argtypes = [_P(AttnShape), ctypes.c_int32, ctypes.c_int32, _P(ctypes.c_size_t)]
 _lib.oda_attn_workspace_size.restype = ctypes.c_int
 _lib.oda_local_decode_attn.argtypes = [_P(AttnShape), _P(AttnInputs), ctypes.c_int32, ctypes.c_int32,
@@ -86,6 +96,17 @@ _lib.oda_commit_kv.argtypes = [_P(AttnShape), ctypes.c_void_p, ctypes.c_void_p, 
                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                ctypes.c_int32, ctypes.c_void_p]
 _lib.oda_commit_kv.restype = ctypes.c_int
+_lib.oda_dense_bf16.argtypes = [_P(DenseDesc), ctypes.c_int32, _V, _V, _V, _V, _V, _V]
+_lib.oda_dense_bf16.restype = ctypes.c_int
+_lib.oda_qk_norm_rope.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _V, _V, _V,
+                                  ctypes.c_float, ctypes.c_double, _V, _V, _V, _V, _V, _V, _V]
+_lib.oda_qk_norm_rope.restype = ctypes.c_int
+_lib.oda_embed_bf16.argtypes = [_V, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _V, _V, _V]
+_lib.oda_embed_bf16.restype = ctypes.c_int
+_lib.oda_copy_rows.argtypes = [ctypes.c_int32, ctypes.c_int32, _V, _V, _V, _V, _V]
+_lib.oda_copy_rows.restype = ctypes.c_int
+_lib.oda_argmax.argtypes = [ctypes.c_int32, ctypes.c_int32, _V, _V, _V]
+_lib.oda_argmax.restype = ctypes.c_int
 _lib.oda_status_string.argtypes = [ctypes.c_int]
 _lib.oda_status_string.restype = ctypes.c_char_p
 _lib.oda_last_error.argtypes = []
@@ -216,6 +237,40 @@ def commit_kv(shape: Shape, k_cache, v_cache, block_table, seq_lens, k_local, v_
                               _ptr(flags), 1 if advance else 0, _stream(stream)))
 
 
+def dense_desc(in_features: int, out_features: int, mode: int, weight, norm_gain=None,
+               rms_eps: float = 1e-6) -> DenseDesc:
+    """The C dense-layer description; it keeps the weight and gain tensors alive."""
+    s = DenseDesc(in_features, out_features, mode, float(rms_eps), _ptr(weight), _ptr(norm_gain))
+    s._keep = (weight, norm_gain)
+    return s
+
+
+def dense_bf16(desc: DenseDesc, batch: int, x, residual, y, work_list=None, n_work=None, stream=None) -> None:
+    _check(_lib.oda_dense_bf16(ctypes.byref(desc), batch, _ptr(x), _ptr(residual), _ptr(y), _ptr(work_list),
+                               _ptr(n_work), _stream(stream)))
+
+
+def qk_norm_rope(batch: int, num_q_heads: int, num_kv_heads: int, head_dim: int, qkv, q_gain, k_gain,
+                 rms_eps: float, rope_theta: float, seq_lens, q_out, k_out, v_out, work_list=None, n_work=None,
+                 stream=None) -> None:
+    _check(_lib.oda_qk_norm_rope(batch, num_q_heads, num_kv_heads, head_dim, _ptr(qkv), _ptr(q_gain),
+                                 _ptr(k_gain), float(rms_eps), float(rope_theta), _ptr(seq_lens), _ptr(q_out),
+                                 _ptr(k_out), _ptr(v_out), _ptr(work_list), _ptr(n_work), _stream(stream)))
+
+
+def embed_bf16(table, vocab: int, d_model: int, batch: int, tokens, x, stream=None) -> None:
+    _check(_lib.oda_embed_bf16(_ptr(table), vocab, d_model, batch, _ptr(tokens), _ptr(x), _stream(stream)))
+
+
+def copy_rows(batch: int, row_len: int, src, dst, work_list=None, n_work=None, stream=None) -> None:
+    _check(_lib.oda_copy_rows(batch, row_len, _ptr(src), _ptr(dst), _ptr(work_list), _ptr(n_work),
+                              _stream(stream)))
+
+
+def argmax(batch: int, n: int, x, index, stream=None) -> None:
+    _check(_lib.oda_argmax(batch, n, _ptr(x), _ptr(index), _stream(stream)))
+
+
 # ---------------------------------------------------------------------------
 # pre-marshalled calls (for tight launch loops: no per-call conversion)
 # ---------------------------------------------------------------------------
@@ -271,3 +326,34 @@ def prepare_commit(shape: Shape, k_cache, v_cache, block_table, seq_lens, k_loca
             _ptr(v_local), _ptr(k_full), _ptr(v_full), _ptr(flags), 1 if advance else 0, _stream(stream))
     return Call(_lib.oda_commit_kv, args, (cs, k_cache, v_cache, block_table, seq_lens, k_local, v_local, k_full,
                                           v_full, flags))
+
+
+def prepare_dense(desc: DenseDesc, batch: int, x, residual, y, work_list=None, n_work=None, stream=None) -> Call:
+    args = (ctypes.byref(desc), batch, _ptr(x), _ptr(residual), _ptr(y), _ptr(work_list), _ptr(n_work),
+            _stream(stream))
+    return Call(_lib.oda_dense_bf16, args, (desc, x, residual, y, work_list, n_work))
+
+
+def prepare_qk_norm_rope(batch: int, num_q_heads: int, num_kv_heads: int, head_dim: int, qkv, q_gain, k_gain,
+                         rms_eps: float, rope_theta: float, seq_lens, q_out, k_out, v_out, work_list=None,
+                         n_work=None, stream=None) -> Call:
+    args = (batch, num_q_heads, num_kv_heads, head_dim, _ptr(qkv), _ptr(q_gain), _ptr(k_gain), float(rms_eps),
+            float(rope_theta), _ptr(seq_lens), _ptr(q_out), _ptr(k_out), _ptr(v_out), _ptr(work_list),
+            _ptr(n_work), _stream(stream))
+    return Call(_lib.oda_qk_norm_rope, args, (qkv, q_gain, k_gain, seq_lens, q_out, k_out, v_out, work_list,
+                                              n_work))
+
+
+def prepare_embed(table, vocab: int, d_model: int, batch: int, tokens, x, stream=None) -> Call:
+    args = (_ptr(table), vocab, d_model, batch, _ptr(tokens), _ptr(x), _stream(stream))
+    return Call(_lib.oda_embed_bf16, args, (table, tokens, x))
+
+
+def prepare_copy_rows(batch: int, row_len: int, src, dst, work_list=None, n_work=None, stream=None) -> Call:
+    args = (batch, row_len, _ptr(src), _ptr(dst), _ptr(work_list), _ptr(n_work), _stream(stream))
+    return Call(_lib.oda_copy_rows, args, (src, dst, work_list, n_work))
+
+
+def prepare_argmax(batch: int, n: int, x, index, stream=None) -> Call:
+    args = (batch, n, _ptr(x), _ptr(index), _stream(stream))
+    return Call(_lib.oda_argmax, args, (x, index))

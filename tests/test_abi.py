@@ -158,3 +158,42 @@ def test_commit_rejects_bad_arguments(L):
     with pytest.raises(L.OdaError) as e:
         call({}, shape=_shape(L, head_dim=96))
     assert e.value.status == -3
+
+
+def test_decoder_entry_points_reject_bad_arguments(L):
+    def status_of(fn):
+        with pytest.raises(L.OdaError) as e:
+            fn()
+        return e.value.status
+
+    w, x, y = 0x10000, 0x20000, 0x30000
+    ok = dict(in_features=64, out_features=8, mode=L.DENSE_PLAIN, weight=w, norm_gain=None)
+
+    def dense(batch=2, x_=x, res=None, wl=None, nw=None, **kw):
+        a = dict(ok)
+        a.update(kw)
+        d = L.dense_desc(a["in_features"], a["out_features"], a["mode"], a["weight"], a["norm_gain"])
+        return lambda: L.dense_bf16(d, batch, x_, res, y, wl, nw, stream=0)
+
+    assert status_of(dense(weight=None)) == -1
+    assert status_of(dense(x_=None)) == -1
+    assert status_of(dense(wl=0x40000)) == -1                 # list without its count
+    assert status_of(dense(in_features=60)) == -2             # K not a multiple of 8
+    assert status_of(dense(batch=0)) == -2
+    assert status_of(dense(mode=7)) == -3
+    assert status_of(dense(mode=L.DENSE_SWIGLU, res=x)) == -3
+    assert status_of(dense(x_=x + 4)) == -2                   # misaligned input
+    rope = lambda **kw: (lambda: L.qk_norm_rope(**{**dict(batch=2, num_q_heads=8, num_kv_heads=2, head_dim=128,
+                                                              qkv=x, q_gain=None, k_gain=None, rms_eps=1e-6,
+                                                              rope_theta=1e6, seq_lens=0x50000, q_out=y,
+                                                              k_out=0x60000, v_out=0x70000, stream=0), **kw}))
+    assert status_of(rope(qkv=None)) == -1
+    assert status_of(rope(num_q_heads=7)) == -2
+    assert status_of(rope(head_dim=256)) == -3
+    assert status_of(rope(rope_theta=1.0)) == -2
+    assert status_of(lambda: L.embed_bf16(w, 100, 60, 2, 0x50000, x, stream=0)) == -2
+    assert status_of(lambda: L.embed_bf16(None, 100, 64, 2, 0x50000, x, stream=0)) == -1
+    assert status_of(lambda: L.copy_rows(2, 6, x, y, stream=0)) == -2
+    assert status_of(lambda: L.copy_rows(2, 8, x, y, 0x40000, None, stream=0)) == -1
+    assert status_of(lambda: L.argmax(2, 10, x, y, stream=0)) == -2
+    assert status_of(lambda: L.argmax(0, 8, x, y, stream=0)) == -2
