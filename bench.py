@@ -15,7 +15,16 @@ weights at the start of a step; "warm" numbers run the K steps back to back.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config llama3-8b] [--head paper|mlp]
 
-Prints one JSON line (see the design doc for the fields).
+Prints one JSON line: the headline value (µs per step at the recall rate
+nearest 0.1), the per-rate sweep for both recall heads, the decode loop, the
+roofline of the dominant kernel and the CPU oracle baseline.
+
+    python bench.py --decoder [--lengths 4139,15918,...]
+
+instead times whole decode steps of a synthetic Qwen3-1.7B-shaped decoder
+(App. A.6's cost model: backbone, attention, recall head, output) at batch
+one: native Full, standalone Local and ODA with the first 2, 4 or 8 of every
+16 steps prescribed Full, as tokens/s, and prints one JSON line of those.
 """
 from __future__ import annotations
 
@@ -457,6 +466,154 @@ def run_sweep(b, wl, args, full_us):
     return sweep
 
 
+PAPER_LENGTHS = (4139, 15918, 31400, 63852, 128852, 261696, 516788)
+
+
+def decoder_bench(args):
+    """Tokens/s of whole decode steps (Alg. 1 with the commit of App. A.5) on a
+    synthetic Qwen3-1.7B-shaped decoder at batch one, per context length:
+    native Full, standalone Local, ODA with a prescribed schedule (the first
+    2 / 4 / 8 of every 16 steps Full, App. B.7; the recall head still runs
+    every step).  Each step is launched as HIP graphs: ODA replays its local
+    stage, reads the device's count of flagged requests into pinned host
+    memory (one host synchronisation per step, the branch of Alg. 1), replays
+    the Full-retry stage only if that count is nonzero, then the output stage
+    (also timed: one graph per step with the retry stage always replayed,
+    whose kernels exit early when nothing is flagged)."""
+    import torch
+
+    import oda_synth as S
+    import paper_2609_20734_amd as P
+    from paper_2609_20734_amd import decoder as PD
+
+    dev = torch.device("cuda:0")
+    shape = PD.QWEN3_1_7B
+    L, d, Hq, Hkv, D = shape.num_layers, shape.d_model, shape.num_q_heads, shape.num_kv_heads, shape.head_dim
+    lengths = [int(x) for x in args.lengths.split(",")] if args.lengths else list(PAPER_LENGTHS)
+    warm, T, period = 16, args.decoder_steps, 16
+    n_sink, window = 4, 2048
+    margin = warm + T + 16
+    cap_blocks = int(math.ceil((max(lengths) + margin) / 16))
+    kv_bytes = 2 * L * cap_blocks * Hkv * D * 16 * 2
+    free, _ = torch.cuda.mem_get_info()
+    log(f"[decoder] Qwen3-1.7B shape, weights {shape.weight_bytes() / 1e9:.2f} GB/forward, KV {kv_bytes / 1e9:.1f} GB, "
+        f"free {free / 1e9:.1f} GB")
+    if kv_bytes + 8e9 > free:
+        raise SystemExit("not enough device memory for the longest context")
+    w = S.decoder_weights_device(args.seed, L, d, Hq, Hkv, D, shape.d_ffn, shape.vocab, dev)
+    k_cache = torch.empty((L, cap_blocks, Hkv, D // 8, 16, 8), dtype=torch.bfloat16, device=dev)
+    v_cache = torch.empty((L, cap_blocks, Hkv, D, 16), dtype=torch.bfloat16, device=dev)
+    for i, t in enumerate((k_cache, v_cache)):
+        for l in range(L):
+            S.fill_normal_bf16_(t[l], args.seed + 31 * l, S.STREAM_K + i)
+            if l % 7 == 6:
+                torch.cuda.synchronize()
+                log(f"[decoder] filled {'KV'[i]} cache layers 0..{l}")
+    dt = 1024                                        # App. A.2 head for d = 2048: 28,325,889 parameters
+    gparams = torch.from_numpy(S.gate_params(args.seed, "paper", d, dt)).to(dev)
+    gate = P.gate_desc(P.HEAD_PAPER, d, dt, gparams, 1e-6)
+    cont = torch.from_numpy(S.tokens(args.seed, warm + T, 1, shape.vocab)).to(dev)
+    n_host = torch.zeros(1, dtype=torch.int32).pin_memory()
+    results = []
+    for n in lengths:
+        nblk = int(math.ceil((n + margin) / 16))
+        perm = S.rng(args.seed + n, S.STREAM_TABLE).permutation(cap_blocks)[:nblk].astype(np.int32)
+        table = torch.from_numpy(perm[None, :]).to(dev)
+        seq0 = torch.tensor([n + 1], dtype=torch.int32, device=dev)     # prompt of n tokens + the current one
+        seq = seq0.clone()
+        dec = PD.Decoder(shape, w, 1, k_cache, v_cache, table, seq, nblk, n + margin, cap_blocks, n_sink, window,
+                         gate=gate, tau=0.0, prescribed=True)
+        row = {"input_tokens": n}
+
+        def capture(i_stage, make):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for c in make()[i_stage]:
+                    c()
+            return g
+
+        def capture_all(make):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for st in make():
+                    for c in st:
+                        c()
+            return g
+
+        def timed(step_fn, sched):
+            seq.copy_(seq0)
+            dec.counter.zero_()
+            torch.cuda.synchronize()
+            for t in range(warm):
+                step_fn(t, sched)
+            torch.cuda.synchronize()
+            seq.copy_(seq0)
+            dec.counter.zero_()
+            a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            a.record()
+            for t in range(T):
+                step_fn(warm + t, sched)
+            b_.record()
+            torch.cuda.synchronize()
+            return a.elapsed_time(b_) / 1e3, int(dec.counter.item())
+
+        def set_inputs(t, sched):
+            dec.tokens.copy_(cont[t])
+            if sched is not None:
+                dec.forced.copy_(sched[t % period])
+
+        for name, make in (("full", dec.full_stages), ("local", dec.local_stages)):
+            g = capture_all(make)
+
+            def step(t, sched, g=g):
+                set_inputs(t, None)
+                g.replay()
+            secs, _ = timed(step, None)
+            row[f"{name}_tps"] = T / secs
+            del g
+        g_loc, g_retry, g_out = (capture(i, dec.oda_stages) for i in range(3))
+        g_all = capture_all(dec.oda_stages)
+        for k in (2, 4, 8):
+            sched = torch.from_numpy(S.periodic_schedule(period, k).astype(np.int32).reshape(period, 1)).to(dev)
+
+            def step_host(t, sched):
+                set_inputs(t, sched)
+                g_loc.replay()
+                n_host.copy_(dec.n_work, non_blocking=True)
+                torch.cuda.current_stream().synchronize()
+                if int(n_host[0]) > 0:
+                    g_retry.replay()
+                g_out.replay()
+
+            def step_dev(t, sched):
+                set_inputs(t, sched)
+                g_all.replay()
+            secs, rec = timed(step_host, sched)
+            row[f"oda{k}_tps"] = T / secs
+            row[f"oda{k}_full_calls"] = rec
+            secs, rec2 = timed(step_dev, sched)
+            row[f"oda{k}_device_only_tps"] = T / secs
+            assert rec == rec2 == k * T // period, (rec, rec2)
+        del g_loc, g_retry, g_out, g_all
+        for key in list(row):
+            if key.endswith("_tps"):
+                row[key] = round(row[key], 2)
+        for k in (2, 4, 8):
+            row[f"oda{k}_speedup"] = round(row[f"oda{k}_tps"] / row["full_tps"], 3)
+        row["local_speedup"] = round(row["local_tps"] / row["full_tps"], 3)
+        log(f"[decoder] n={n}: Full {row['full_tps']:.1f} tok/s, Local {row['local_tps']:.1f}, "
+            + ", ".join(f"ODA {100 * k // 16}% {row[f'oda{k}_tps']:.1f} (x{row[f'oda{k}_speedup']:.2f}; "
+                        f"device-only {row[f'oda{k}_device_only_tps']:.1f})" for k in (2, 4, 8)))
+        results.append(row)
+        del dec
+    print(json.dumps({"decoder": {"model": "Qwen3-1.7B-shaped synthetic decoder (28 x 2048, 16q/8kv x 128, "
+                                           "SwiGLU 6144, vocab 151936, bf16 weights)",
+                                  "batch": 1, "local": {"sinks": n_sink, "window": window},
+                                  "recall_head": "App. A.2, 2048 -> 1024", "steps": T, "warmup": warm,
+                                  "weight_bytes_per_forward": shape.weight_bytes(), "rows": results}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -471,6 +628,10 @@ def main():
     ap.add_argument("--one-head", action="store_true", help="skip the second recall head's sweep")
     ap.add_argument("--no-loop", action="store_true", help="skip the growing-context decode loop (graph) section")
     ap.add_argument("--loop-only", action="store_true", help="only the decode loop section (for profiling)")
+    ap.add_argument("--decoder", action="store_true",
+                    help="time whole steps of the synthetic decoder (tokens/s) instead of the attention path")
+    ap.add_argument("--lengths", default="", help="--decoder: comma-separated context lengths")
+    ap.add_argument("--decoder-steps", type=int, default=64, help="--decoder: timed steps per method")
     ap.add_argument("--roofline-only", action="store_true",
                     help="only the roofline leg (always-Full calls) plus a 1 GiB copy, for PMC profiling")
     args = ap.parse_args()
@@ -478,6 +639,10 @@ def main():
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}), flush=True)
         sys.exit(2)
+
+    if args.decoder:
+        decoder_bench(args)
+        return
 
     import torch
 

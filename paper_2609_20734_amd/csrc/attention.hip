@@ -653,8 +653,8 @@ void make_plan(const oda_attn_shape* s, int n_sink, int window, Plan* p) {
   p->dyn = 0;
   if (bps == 0) {
     const int64_t want = oda::ceil_div(ODA_TARGET_GROUPS, units_per_request);
-    // at least 4 blocks per wavefront
-    const int64_t max_split = std::max<int64_t>(1, nvb / (4 * kWaves));
+    // at least one block pair per wavefront
+    const int64_t max_split = std::max<int64_t>(1, nvb / (2 * kWaves));
     const int64_t nsplit = std::max<int64_t>(1, std::min(want, max_split));
     bps = oda::round_up(oda::ceil_div(nvb, nsplit), 2);
     p->dyn = 1;

@@ -33,6 +33,10 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kWaves = 4;
 constexpr int kTile = 8;   // most requests per wavefront in a dense layer
 
+#ifndef ODA_DENSE_MIN_WAVES
+#define ODA_DENSE_MIN_WAVES 2048   // grouping rows stops short of fewer wavefronts than this
+#endif
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 __device__ __forceinline__ uint16_t to_bf16(float f) {   // round to nearest, ties to even
@@ -72,52 +76,63 @@ struct DenseArgs {
   float eps;
 };
 
-// One wavefront per (output row, tile of up to T selected requests).  Lanes
-// take 8 consecutive weights each (one 16-byte load), so a wavefront reads
-// 1 KiB of the row per step, several steps in flight; the inputs come from
-// cache.  The input's sum of squares (for RMSNorm) accumulates in the same
-// pass.  T = 1 for a single request keeps the registers for loads in flight.
-template <bool kSwiGLU, int T>
+// One wavefront per (group of R output rows, tile of up to T selected
+// requests).  Lanes take 8 consecutive weights of each row (one 16-byte load
+// per row), so a wavefront reads R KiB per 512-element chunk, several chunks
+// in flight; every input load serves all R rows.  The inputs come from cache.
+// The input's sum of squares (for RMSNorm) accumulates in the same pass.
+// Small T keeps registers for loads in flight; R > 1 makes the wavefronts of
+// a layer with many short rows fewer and longer.
+template <bool kSwiGLU, int T, int R>
 __global__ __launch_bounds__(256) void dense_kernel(DenseArgs p) {
-  constexpr int kTile = T;
+  constexpr int kAcc = R * T;
+  static_assert(kAcc <= 64, "one result per lane");
   const int lane = threadIdx.x & 63;
   const int wave = uniform(threadIdx.x >> 6);
   const int item = blockIdx.x * kWaves + wave;
-  const int row = item % p.N;
-  const int s0 = (item / p.N) * kTile;
+  const int groups = p.N / R;                  // the host keeps N a multiple of R
+  const int row0 = (item % groups) * R;
+  const int s0 = (item / groups) * T;
   const int count = selected_count(p.n_work, p.B);
   if (s0 >= count) return;
-  const int nb = min(kTile, count - s0);
+  const int nb = min(T, count - s0);
   const int my_req = lane < nb ? selected_request(p.work_list, s0 + lane) : 0;
-  int req[kTile];
+  int req[T];
 #pragma unroll
-  for (int bi = 0; bi < kTile; ++bi) req[bi] = __shfl(my_req, bi);
+  for (int bi = 0; bi < T; ++bi) req[bi] = __shfl(my_req, bi);
   const bool norm = p.gain != nullptr;
 
-  const uint16_t* wrow = p.W + (int64_t)row * p.K;
-  const uint16_t* wrow2 = kSwiGLU ? p.W + (int64_t)(p.N + row) * p.K : nullptr;
-  float acc[kTile], acc2[kSwiGLU ? kTile : 1], ss[kTile];
+  const uint16_t* wrow = p.W + (int64_t)row0 * p.K;
+  const uint16_t* wrow2 = kSwiGLU ? p.W + (int64_t)(p.N + row0) * p.K : nullptr;
+  float acc[R][T], acc2[kSwiGLU ? R : 1][T], ss[T];
 #pragma unroll
-  for (int bi = 0; bi < kTile; ++bi) {
-    acc[bi] = 0.f;
+  for (int bi = 0; bi < T; ++bi) {
     ss[bi] = 0.f;
-    if (kSwiGLU) acc2[bi] = 0.f;
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      acc[j][bi] = 0.f;
+      if (kSwiGLU) acc2[j][bi] = 0.f;
+    }
   }
-  // 512-element chunks (8 per lane), several in flight.  In a ragged last
-  // chunk the lanes past K read element 0 again and weigh it by zero, so
-  // every load is unconditional and the loads of successive chunks overlap.
+  // 512-element chunks (8 per lane).  In a ragged last chunk the lanes past K
+  // read element 0 again and weigh it by zero, so every load is unconditional
+  // and the loads of successive chunks overlap.
   const int nchunks = (p.K + 511) / 512;
-  // about eight 16-byte weight loads in flight per lane (SwiGLU reads two rows)
-  constexpr int kUnroll = kSwiGLU ? (T == 1 ? 4 : 2) : (T == 1 ? 8 : 4);
+  // about eight 16-byte weight loads in flight per lane
+  constexpr int kRowsPerChunk = kSwiGLU ? 2 * R : R;
+  constexpr int kUnroll = kRowsPerChunk >= 8 ? 1 : 8 / kRowsPerChunk;
 #pragma unroll kUnroll
   for (int c = 0; c < nchunks; ++c) {
     const int k0 = c * 512 + 8 * lane;
     const bool in = k0 < p.K;
     const int k = in ? k0 : 0;
     const float mask = in ? 1.f : 0.f;
-    const u32x4 w = *reinterpret_cast<const u32x4*>(wrow + k);
-    u32x4 w2 = {0u, 0u, 0u, 0u};
-    if (kSwiGLU) w2 = *reinterpret_cast<const u32x4*>(wrow2 + k);
+    u32x4 w[R], w2[kSwiGLU ? R : 1];
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      w[j] = *reinterpret_cast<const u32x4*>(wrow + (int64_t)j * p.K + k);
+      if (kSwiGLU) w2[j] = *reinterpret_cast<const u32x4*>(wrow2 + (int64_t)j * p.K + k);
+    }
     float g[8];
     if (norm) {
       const float4 g0 = *reinterpret_cast<const float4*>(p.gain + k);
@@ -129,7 +144,7 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs p) {
       for (int e = 0; e < 8; ++e) g[e] = 1.f;
     }
 #pragma unroll
-    for (int bi = 0; bi < kTile; ++bi) {
+    for (int bi = 0; bi < T; ++bi) {
       if (bi < nb) {
         const float* xr = p.x + (int64_t)req[bi] * p.K + k;
         const float4 x0 = *reinterpret_cast<const float4*>(xr);
@@ -140,30 +155,42 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs p) {
         for (int e = 0; e < 8; ++e) {
           if (norm) ss[bi] += xv[e] * xv[e];
           const float xg = xv[e] * g[e];
-          const uint32_t we = w[e >> 1], we2 = w2[e >> 1];
-          acc[bi] += ((e & 1) ? bf16_hi(we) : bf16_lo(we)) * xg;
-          if (kSwiGLU) acc2[bi] += ((e & 1) ? bf16_hi(we2) : bf16_lo(we2)) * xg;
+#pragma unroll
+          for (int j = 0; j < R; ++j) {
+            const uint32_t we = w[j][e >> 1];
+            acc[j][bi] += ((e & 1) ? bf16_hi(we) : bf16_lo(we)) * xg;
+            if (kSwiGLU) {
+              const uint32_t we2 = w2[j][e >> 1];
+              acc2[j][bi] += ((e & 1) ? bf16_hi(we2) : bf16_lo(we2)) * xg;
+            }
+          }
         }
       }
     }
   }
 
+  // reduce over the wavefront; lane j * T + bi keeps row row0 + j, request bi
   float v = 0.f, v2 = 0.f, my_ss = 0.f;
 #pragma unroll
-  for (int bi = 0; bi < kTile; ++bi) {
+  for (int bi = 0; bi < T; ++bi) {
     if (bi < nb) {
-      const float a = wave_sum(acc[bi]);
-      const float a2 = kSwiGLU ? wave_sum(acc2[bi]) : 0.f;
       const float s = norm ? wave_sum(ss[bi]) : 0.f;
-      if (lane == bi) {
-        v = a;
-        v2 = a2;
-        my_ss = s;
+#pragma unroll
+      for (int j = 0; j < R; ++j) {
+        const float a = wave_sum(acc[j][bi]);
+        const float a2 = kSwiGLU ? wave_sum(acc2[j][bi]) : 0.f;
+        if (lane == j * T + bi) {
+          v = a;
+          v2 = a2;
+          my_ss = s;
+        }
       }
     }
   }
-  if (lane >= nb) return;
-  const int b = my_req;
+  const int j = lane / T, bi = lane % T;
+  if (lane >= kAcc || bi >= nb) return;
+  const int b = selected_request(p.work_list, s0 + bi);
+  const int row = row0 + j;
   const float inv = norm ? rsqrtf(my_ss / (float)p.K + p.eps) : 1.f;
   float out;
   if (kSwiGLU) {
@@ -358,26 +385,54 @@ extern "C" oda_status oda_dense_bf16(const oda_dense_desc* desc, int32_t batch, 
   if (!(desc->rms_eps >= 0.f) || !std::isfinite(desc->rms_eps)) return oda::fail(ODA_ERR_SHAPE, "rms_eps must be >= 0");
   if (!oda::aligned(desc->weight, 16) || !oda::aligned(x, 16) || (desc->norm_gain && !oda::aligned(desc->norm_gain, 16)))
     return oda::fail(ODA_ERR_SHAPE, "weight, x and norm_gain must be 16-byte aligned");
-  // requests per wavefront: one, up to four, or up to eight
+  // requests per wavefront: one, up to four, or up to eight; then the most
+  // rows per wavefront that still leave >= ODA_DENSE_MIN_WAVES wavefronts
   const int tile = batch == 1 ? 1 : batch <= 4 ? 4 : kTile;
-  const int64_t items = (int64_t)desc->out_features * oda::ceil_div(batch, tile);
-  const int64_t groups = oda::ceil_div(items, kWaves);
-  if (groups > INT_MAX) return oda::fail(ODA_ERR_SHAPE, "layer too large");
-  DenseArgs a{desc->weight, desc->norm_gain, x, residual, y, work_list, n_work,
-              desc->out_features, desc->in_features, batch, desc->rms_eps};
-  const dim3 grid((unsigned)groups), block(256);
+  const int64_t tiles = oda::ceil_div(batch, tile);
+  const int N = desc->out_features;
   const bool swiglu = desc->mode == ODA_DENSE_SWIGLU;
+  const int rmax = swiglu ? (tile == 1 ? 4 : 2) : (tile == 1 ? 8 : tile == 4 ? 4 : 2);
+  int rows = 1;
+  for (int r = rmax; r > 1; r /= 2)
+    if (N % r == 0 && (int64_t)(N / r) * tiles >= ODA_DENSE_MIN_WAVES) {
+      rows = r;
+      break;
+    }
+  const int64_t groups = oda::ceil_div((int64_t)(N / rows) * tiles, kWaves);
+  if (groups > INT_MAX) return oda::fail(ODA_ERR_SHAPE, "layer too large");
+  DenseArgs a{desc->weight, desc->norm_gain, x, residual, y, work_list, n_work, N, desc->in_features, batch,
+              desc->rms_eps};
+  const dim3 grid((unsigned)groups), block(256);
   (void)hipGetLastError();
-  if (tile == 1) {
-    if (swiglu) hipLaunchKernelGGL((dense_kernel<true, 1>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((dense_kernel<false, 1>), grid, block, 0, stream, a);
-  } else if (tile == 4) {
-    if (swiglu) hipLaunchKernelGGL((dense_kernel<true, 4>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((dense_kernel<false, 4>), grid, block, 0, stream, a);
+#define ODA_DENSE_LAUNCH(SW, T, R) hipLaunchKernelGGL((dense_kernel<SW, T, R>), grid, block, 0, stream, a)
+  if (swiglu) {
+    if (tile == 1) {
+      if (rows == 4) ODA_DENSE_LAUNCH(true, 1, 4);
+      else if (rows == 2) ODA_DENSE_LAUNCH(true, 1, 2);
+      else ODA_DENSE_LAUNCH(true, 1, 1);
+    } else if (tile == 4) {
+      if (rows == 2) ODA_DENSE_LAUNCH(true, 4, 2);
+      else ODA_DENSE_LAUNCH(true, 4, 1);
+    } else {
+      if (rows == 2) ODA_DENSE_LAUNCH(true, kTile, 2);
+      else ODA_DENSE_LAUNCH(true, kTile, 1);
+    }
   } else {
-    if (swiglu) hipLaunchKernelGGL((dense_kernel<true, kTile>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((dense_kernel<false, kTile>), grid, block, 0, stream, a);
+    if (tile == 1) {
+      if (rows == 8) ODA_DENSE_LAUNCH(false, 1, 8);
+      else if (rows == 4) ODA_DENSE_LAUNCH(false, 1, 4);
+      else if (rows == 2) ODA_DENSE_LAUNCH(false, 1, 2);
+      else ODA_DENSE_LAUNCH(false, 1, 1);
+    } else if (tile == 4) {
+      if (rows == 4) ODA_DENSE_LAUNCH(false, 4, 4);
+      else if (rows == 2) ODA_DENSE_LAUNCH(false, 4, 2);
+      else ODA_DENSE_LAUNCH(false, 4, 1);
+    } else {
+      if (rows == 2) ODA_DENSE_LAUNCH(false, kTile, 2);
+      else ODA_DENSE_LAUNCH(false, kTile, 1);
+    }
   }
+#undef ODA_DENSE_LAUNCH
   return launch_status();
 }
 
