@@ -12,11 +12,15 @@
 // folded into the same pass (the sum of squares is accumulated next to the
 // dot products), so normalised inputs are never stored.
 //
-// The layers of the head are dependent launches on one stream.  A single
-// launch stepping through the layers with a barrier over its workgroups was
-// slower on this part: publishing each layer's results across the chip's L2
-// slices needs a write-back and an invalidate per workgroup per layer, which
-// costs more than a kernel boundary.
+// The layers of the head are dependent launches on one stream.  For one or
+// two requests with towers up to 512 wide, each residual SwiGLU block is a
+// single launch (its hidden units split over the workgroups, the down
+// projection left as partial sums that the next launch adds in a fixed
+// order): five launches instead of seven.  A single launch stepping through
+// the layers with a barrier over its workgroups was slower on this part:
+// publishing each layer's results across the chip's L2 slices needs a
+// write-back and an invalidate per workgroup per layer, which costs more than
+// a kernel boundary.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -272,6 +276,54 @@ __global__ __launch_bounds__(256) void gate_fusion_kernel(LinArgs p) {
   p.Y[(int64_t)b * p.rows + row] = 0.5f * (s3 + silu(mine + p.bias[row]));
 }
 
+constexpr int kSplitMaxB = 2;         // batches up to this size may take the split-hidden blocks
+constexpr int kSplitMaxDt = 512;      // tower widths up to this take them (two 256-wide chunks per row)
+constexpr int kSplitMaxHs = 16;       // hidden units per workgroup (4 per wavefront)
+
+// out[e] = base[e] + sum_w parts[w][e] for e < n (n a multiple of 4, n / 4 <=
+// kSplitMaxB * kSplitMaxDt / 4), into LDS, by a workgroup of exactly NT threads:
+// groups of threads take interleaved partials, eight loads in flight each,
+// and the group sums are then added in group order (a fixed order).
+template <int NT>
+__device__ __forceinline__ void sum_parts(const float* base, const float* parts, int nparts, int n, float* out,
+                                          float4* scratch) {
+  const int C = n / 4;
+  const int Cg = min(C, NT);
+  const int G = NT / Cg;
+  const int t = threadIdx.x;
+  const int g = t / Cg, cl = t % Cg;
+  if (g < G) {
+    for (int c = cl; c < C; c += Cg) {
+      float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int w0 = g; w0 < nparts; w0 += 8 * G) {
+        float4 v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int w = w0 + i * G;
+          v[i] = w < nparts ? *reinterpret_cast<const float4*>(parts + (int64_t)w * n + 4 * c)
+                            : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc = make_float4(acc.x + v[i].x, acc.y + v[i].y, acc.z + v[i].z, acc.w + v[i].w);
+      }
+      scratch[g * C + c] = acc;
+    }
+  }
+  __syncthreads();
+  for (int c = t; c < C; c += NT) {
+    float4 v = *reinterpret_cast<const float4*>(base + 4 * c);
+    for (int gg = 0; gg < G; ++gg) {
+      const float4 u = scratch[gg * C + c];
+      v = make_float4(v.x + u.x, v.y + u.y, v.z + u.z, v.w + u.w);
+    }
+    *reinterpret_cast<float4*>(out + 4 * c) = v;
+  }
+  __syncthreads();
+}
+
+// LDS float4 slots sum_parts needs: max(NT, n / 4)
+constexpr int kPartsScratch = kSplitMaxB * kSplitMaxDt / 4;
+
 struct FinalArgs {
   const float* X;       // [B][K]: z2 (paper head) or the MLP hidden layer
   const float* gain;    // paper head: final RMSNorm gain [K]; MLP: NULL
@@ -283,6 +335,8 @@ struct FinalArgs {
   int32_t* work_list;
   int32_t* n_work;
   int64_t* counter;
+  const float* parts;   // NULL, or [nparts][B][K] partial sums added to X (split-hidden blocks)
+  int nparts;
   int K, B;
   float eps, tau;
 };
@@ -295,9 +349,16 @@ constexpr int kFinalWaves = 16;
 // requests (ballot + prefix popcount) by wavefront 0.
 __global__ __launch_bounds__(kFinalWaves * 64) void gate_final_kernel(FinalArgs p) {
   __shared__ float sm_score[64];
+  __shared__ float sx[kSplitMaxB * kSplitMaxDt];
+  __shared__ float4 sscratch[kPartsScratch > kFinalWaves * 64 ? kPartsScratch : kFinalWaves * 64];
   const int lane = threadIdx.x & 63;
   const int wave = uniform(threadIdx.x >> 6);
   const bool norm = p.gain != nullptr;
+  // split-hidden blocks (B <= kSplitMaxB): z = residual + the last block's
+  // partial sums, formed once in LDS by the whole workgroup
+  const bool parts = p.parts != nullptr;
+  if (parts) sum_parts<kFinalWaves * 64>(p.X, p.parts, p.nparts, p.B * p.K, sx, sscratch);
+  const float* X = parts ? sx : p.X;
   int total = 0;
   for (int c0 = 0; c0 < p.B; c0 += 64) {
     const int nc = min(64, p.B - c0);
@@ -305,7 +366,7 @@ __global__ __launch_bounds__(kFinalWaves * 64) void gate_final_kernel(FinalArgs 
       const int b = c0 + i;
       float dot = 0.f, ss = 0.f;
       for (int k = 4 * lane; k < p.K; k += 256) {
-        const float4 x = *reinterpret_cast<const float4*>(p.X + (int64_t)b * p.K + k);
+        const float4 x = *reinterpret_cast<const float4*>(X + (int64_t)b * p.K + k);
         float4 wk = *reinterpret_cast<const float4*>(p.w + k);
         if (norm) {
           ss += dot4(x, x);
@@ -346,6 +407,126 @@ __global__ __launch_bounds__(kFinalWaves * 64) void gate_final_kernel(FinalArgs 
 }
 
 // ---------------------------------------------------------------------------
+// split-hidden SwiGLU block (small batches)
+// ---------------------------------------------------------------------------
+
+struct SplitArgs {
+  const float* z_base;     // [B][dt]: the block's residual input, before the incoming partial sums
+  const float* parts_in;   // NULL, or [nparts_in][B][dt] partial down sums of the previous block
+  float* z_out;            // NULL, or where workgroup 0 stores z_base + sum(parts_in) (the next residual)
+  const float* gain;       // [dt] the block's RMSNorm gain
+  const float* Wg;         // [2dt][dt]
+  const float* Wu;         // [2dt][dt]
+  const float* Wd;         // [dt][2dt]
+  float* parts_out;        // [gridDim.x][B][dt]
+  int nparts_in, dt, B, hs;
+  float eps;
+};
+
+// One residual SwiGLU block, z_out = z + W_d (SiLU(W_g n) * (W_u n)) with
+// n = RMSNorm(z), in one launch: workgroup w owns hidden units
+// [w hs, (w + 1) hs), computes them from the whole input, and writes its share
+// of the down projection, sum over its units of W_d[:, j] h_j, as a partial
+// sum.  The next launch adds the partial sums in a fixed order, so the block
+// needs no grid-wide barrier and the result does not depend on timing.  The
+// workgroup's weights (HW hidden units per wavefront, KC 256-wide chunks per
+// row, and its W_d columns) are loaded first, so their latency overlaps the
+// gathering of the block input.
+template <int HW, int KC>
+__global__ __launch_bounds__(256) void gate_split_block_kernel(SplitArgs p) {
+  __shared__ float sz[kSplitMaxB * kSplitMaxDt];
+  __shared__ float sh[kSplitMaxB * kSplitMaxHs];
+  __shared__ float sred[kWaves][kSplitMaxB];
+  __shared__ float4 sscratch[kPartsScratch > 256 ? kPartsScratch : 256];
+  const int lane = threadIdx.x & 63;
+  const int wave = uniform(threadIdx.x >> 6);
+  const int n = p.B * p.dt;
+  const int hs = HW * kWaves;
+  const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+  // this workgroup's weights
+  float4 wg[HW][KC], wu[HW][KC], gk[KC], wd[KC][HW];
+  const int j0 = blockIdx.x * hs + wave * HW;
+  const int jb = blockIdx.x * hs;
+#pragma unroll
+  for (int c = 0; c < KC; ++c) {
+    const int k = c * 256 + 4 * lane;
+    const bool in = k < p.dt;
+    gk[c] = in ? *reinterpret_cast<const float4*>(p.gain + k) : zero;
+#pragma unroll
+    for (int jj = 0; jj < HW; ++jj) {
+      wg[jj][c] = in ? *reinterpret_cast<const float4*>(p.Wg + (int64_t)(j0 + jj) * p.dt + k) : zero;
+      wu[jj][c] = in ? *reinterpret_cast<const float4*>(p.Wu + (int64_t)(j0 + jj) * p.dt + k) : zero;
+    }
+    const int r = threadIdx.x + 256 * c;
+#pragma unroll
+    for (int q = 0; q < HW; ++q)
+      wd[c][q] = r < p.dt ? *reinterpret_cast<const float4*>(p.Wd + (int64_t)r * 2 * p.dt + jb + 4 * q) : zero;
+  }
+  // the block input for every request: the residual plus the previous block's partial sums
+  sum_parts<256>(p.z_base, p.parts_in, p.nparts_in, n, sz, sscratch);
+  if (p.z_out != nullptr && blockIdx.x == 0)
+    for (int e = threadIdx.x; e < n; e += 256) p.z_out[e] = sz[e];
+  float inv[kSplitMaxB];
+#pragma unroll
+  for (int b = 0; b < kSplitMaxB; ++b) {
+    float ss = 0.f;
+    if (b < p.B)
+      for (int k = threadIdx.x; k < p.dt; k += 256) ss += sz[b * p.dt + k] * sz[b * p.dt + k];
+    ss = wave_sum(ss);
+    if (lane == 0) sred[wave][b] = ss;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int b = 0; b < kSplitMaxB; ++b) {
+    float t = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) t += sred[w][b];
+    inv[b] = rsqrtf(t / (float)p.dt + p.eps);
+  }
+  // hidden units
+#pragma unroll
+  for (int b = 0; b < kSplitMaxB; ++b) {
+    if (b < p.B) {
+      float4 x[KC];
+#pragma unroll
+      for (int c = 0; c < KC; ++c) {
+        const int k = c * 256 + 4 * lane;
+        x[c] = k < p.dt ? mul4(*reinterpret_cast<const float4*>(sz + b * p.dt + k), gk[c]) : zero;
+      }
+#pragma unroll
+      for (int jj = 0; jj < HW; ++jj) {
+        float g = 0.f, u = 0.f;
+#pragma unroll
+        for (int c = 0; c < KC; ++c) {
+          g += dot4(wg[jj][c], x[c]);
+          u += dot4(wu[jj][c], x[c]);
+        }
+        g = wave_sum(g) * inv[b];
+        u = wave_sum(u) * inv[b];
+        if (lane == 0) sh[b * hs + wave * HW + jj] = silu(g) * u;
+      }
+    }
+  }
+  __syncthreads();
+  // this workgroup's share of the down projection for every output row
+#pragma unroll
+  for (int c = 0; c < KC; ++c) {
+    const int r = threadIdx.x + 256 * c;
+    if (r < p.dt) {
+#pragma unroll
+      for (int b = 0; b < kSplitMaxB; ++b) {
+        if (b < p.B) {
+          float acc = 0.f;
+#pragma unroll
+          for (int q = 0; q < HW; ++q) acc += dot4(wd[c][q], *reinterpret_cast<const float4*>(sh + b * hs + 4 * q));
+          p.parts_out[((int64_t)blockIdx.x * p.B + b) * p.dt + r] = acc;
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
 
@@ -378,8 +559,24 @@ HeadLayout paper_layout(int64_t d, int64_t dt) {
 }
 
 struct GateWs {
-  size_t abc, z0, z1, hdn, hid, bytes;
+  size_t abc, z0, z1, hdn, p1, p2, hid, bytes;
 };
+
+// Workgroups of a split-hidden block (0 if the batch or width does not take
+// that path): 64, or fewer when the hidden width 2 dt has fewer multiples of 4
+// hidden units per workgroup; the partial sums the next launch adds must stay
+// small (<= 256 KiB per consumer workgroup).
+int split_groups(int64_t B, int64_t dt) {
+  if (B > kSplitMaxB || dt > kSplitMaxDt || dt % 4) return 0;
+  for (int nw = 64; nw >= 1; nw /= 2) {
+    if ((2 * dt) % nw) continue;
+    const int64_t hs = 2 * dt / nw;
+    if (hs % kWaves || hs > kSplitMaxHs) continue;
+    if ((int64_t)nw * B * dt * 4 > 256 * 1024) return 0;
+    return nw;
+  }
+  return 0;
+}
 
 GateWs gate_ws_layout(int kind, int64_t B, int64_t dt) {
   GateWs w{};
@@ -394,6 +591,9 @@ GateWs gate_ws_layout(int kind, int64_t B, int64_t dt) {
     w.z0 = take(B * dt);
     w.z1 = take(B * dt);
     w.hdn = take(2 * B * dt);
+    const int nw = split_groups(B, dt);
+    w.p1 = take((int64_t)nw * B * dt);
+    w.p2 = take((int64_t)nw * B * dt);
   } else {
     w.hid = take(B * dt);
   }
@@ -555,37 +755,76 @@ extern "C" oda_status oda_recall_gate(const oda_gate_desc* gate, int32_t batch, 
     a.rows = dt;
     a.K = 9 * dt;
     launch_fusion(a, stream);
-    // two pre-RMSNorm residual SwiGLU blocks
-    float* zin = z0;
-    float* zout = z1;
-    for (int k = 0; k < 2; ++k) {
-      const int64_t base = k * H.block_stride;
-      a = LinArgs{};
-      a.B = batch;
-      a.dt = dt;
-      a.eps = gate->rms_eps;
-      a.W = P + H.blk_gate + base;
-      a.W2 = P + H.blk_up + base;
-      a.gain = P + H.blk_rms + base;
-      a.X[0] = zin;
-      a.Y = hdn;
-      a.rows = 2 * dt;
-      a.K = dt;
-      launch_linear<kGateUp>(a, stream);
-      a = LinArgs{};
-      a.B = batch;
-      a.dt = dt;
-      a.W = P + H.blk_down + base;
-      a.X[0] = hdn;
-      a.aux = zin;
-      a.Y = zout;
-      a.rows = dt;
-      a.K = 2 * dt;
-      launch_linear<kDown>(a, stream);
-      std::swap(zin, zout);
+    const int nw = split_groups(batch, dt);
+    if (nw > 0) {
+      // two split-hidden blocks: z0 -> partials P1 -> (z1 = z0 + P1) -> partials P2;
+      // the score adds P2 to z1
+      float* p1 = reinterpret_cast<float*>(wsb + ws.p1);
+      float* p2 = reinterpret_cast<float*>(wsb + ws.p2);
+      for (int k = 0; k < 2; ++k) {
+        const int64_t base = k * H.block_stride;
+        SplitArgs sa{};
+        sa.z_base = z0;
+        sa.parts_in = k == 0 ? nullptr : p1;
+        sa.nparts_in = k == 0 ? 0 : nw;
+        sa.z_out = k == 0 ? nullptr : z1;
+        sa.gain = P + H.blk_rms + base;
+        sa.Wg = P + H.blk_gate + base;
+        sa.Wu = P + H.blk_up + base;
+        sa.Wd = P + H.blk_down + base;
+        sa.parts_out = k == 0 ? p1 : p2;
+        sa.dt = dt;
+        sa.B = batch;
+        sa.hs = 2 * dt / nw;
+        sa.eps = gate->rms_eps;
+        const int hw = sa.hs / kWaves;
+        const dim3 g((unsigned)nw), t(256);
+        if (dt <= 256) {
+          if (hw == 1) hipLaunchKernelGGL((gate_split_block_kernel<1, 1>), g, t, 0, stream, sa);
+          else if (hw == 2) hipLaunchKernelGGL((gate_split_block_kernel<2, 1>), g, t, 0, stream, sa);
+          else hipLaunchKernelGGL((gate_split_block_kernel<4, 1>), g, t, 0, stream, sa);
+        } else {
+          if (hw == 1) hipLaunchKernelGGL((gate_split_block_kernel<1, 2>), g, t, 0, stream, sa);
+          else if (hw == 2) hipLaunchKernelGGL((gate_split_block_kernel<2, 2>), g, t, 0, stream, sa);
+          else hipLaunchKernelGGL((gate_split_block_kernel<4, 2>), g, t, 0, stream, sa);
+        }
+      }
+      fa.X = z1;
+      fa.parts = p2;
+      fa.nparts = nw;
+    } else {
+      // two pre-RMSNorm residual SwiGLU blocks, one launch per dense layer
+      float* zin = z0;
+      float* zout = z1;
+      for (int k = 0; k < 2; ++k) {
+        const int64_t base = k * H.block_stride;
+        a = LinArgs{};
+        a.B = batch;
+        a.dt = dt;
+        a.eps = gate->rms_eps;
+        a.W = P + H.blk_gate + base;
+        a.W2 = P + H.blk_up + base;
+        a.gain = P + H.blk_rms + base;
+        a.X[0] = zin;
+        a.Y = hdn;
+        a.rows = 2 * dt;
+        a.K = dt;
+        launch_linear<kGateUp>(a, stream);
+        a = LinArgs{};
+        a.B = batch;
+        a.dt = dt;
+        a.W = P + H.blk_down + base;
+        a.X[0] = hdn;
+        a.aux = zin;
+        a.Y = zout;
+        a.rows = dt;
+        a.K = 2 * dt;
+        launch_linear<kDown>(a, stream);
+        std::swap(zin, zout);
+      }
+      fa.X = zin;
     }
     // q = w_o . RMSNorm(z2) + b_o
-    fa.X = zin;
     fa.gain = P + H.rms_o;
     fa.w = P + H.w_o;
     fa.bias = P + H.b_o;
@@ -608,8 +847,9 @@ extern "C" oda_status oda_recall_gate(const oda_gate_desc* gate, int32_t batch, 
     fa.bias = P + (int64_t)dt * d + 2 * dt;
     fa.K = dt;
   }
-  // one wavefront per request in flight, at most kFinalWaves
-  const int final_threads = 64 * std::min(kFinalWaves, batch);
+  // one wavefront per request in flight, at most kFinalWaves; the whole
+  // workgroup when it first adds up the last block's partial sums
+  const int final_threads = fa.parts ? 64 * kFinalWaves : 64 * std::min(kFinalWaves, batch);
   hipLaunchKernelGGL(gate_final_kernel, dim3(1), dim3((unsigned)final_threads), 0, stream, fa);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return oda::fail(ODA_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));

@@ -68,7 +68,9 @@ def _check(g, h, e, l, tau, forced=None):
                                          # launch shapes: K split over a workgroup, grouped rows, ragged
                                          # tiles and chunk tails, wide towers, batches over 64
                                          ("paper", 2048, 1024, 1), ("paper", 4096, 260, 70),
-                                         ("paper", 256, 516, 2), ("mlp", 8192, 512, 8), ("mlp", 4096, 256, 70)])
+                                         ("paper", 256, 516, 2), ("mlp", 8192, 512, 8), ("mlp", 4096, 256, 70),
+                                         # split-hidden SwiGLU blocks (one or two requests)
+                                         ("paper", 1024, 128, 2), ("paper", 4096, 512, 1), ("paper", 256, 32, 2)])
 def test_scores_and_flags(kind, d, dh, B):
     g = Gate(kind, d, dh, B)
     h, e, l = (x[0] for x in S.gate_inputs(3, 1, B, d))
@@ -107,6 +109,13 @@ def test_nonfinite_scores_go_to_full():
         assert fl.tolist() == [0, 1, 0, 0, 1, 0] and wl.tolist() == [1, 4]
         sc, fl, wl, n = g.run(h, e, l, np.inf, forced=np.array([1, 0, 0, 1, 0, 0], np.int32))
         assert fl.tolist() == [1, 1, 0, 1, 1, 0] and n == 4
+    # the split-hidden blocks (two requests): NaN in one request stays in it
+    g = Gate("paper", 256, 64, 2)
+    h, e, l = (x[0].copy() for x in S.gate_inputs(5, 1, 2, 256))
+    h[1, 7] = np.nan
+    sc, fl, wl, n = g.run(h, e, l, np.inf)
+    assert np.isfinite(sc[0]) and not np.isfinite(sc[1])
+    assert fl.tolist() == [0, 1] and wl.tolist() == [1]
 
 
 @pytest.mark.parametrize("k,expected", [(2, 126), (4, 252), (8, 504)])
