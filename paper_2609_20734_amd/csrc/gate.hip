@@ -65,6 +65,14 @@ __device__ __forceinline__ float4 absdiff4(float4 a, float4 b) {
   return make_float4(fabsf(a.x - b.x), fabsf(a.y - b.y), fabsf(a.z - b.z), fabsf(a.w - b.w));
 }
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+// p[0..3] if ok, else zeros.  The load itself is unconditional (from `safe`,
+// any valid address, when !ok) and the value is selected afterwards: a
+// conditional load would make the compiler select between the global
+// address and a stack copy of the zeros (scratch plus flat loads).
+__device__ __forceinline__ float4 load4_or_zero(const float* p, const float* safe, bool ok) {
+  const float4 v = *reinterpret_cast<const float4*>(ok ? p : safe);
+  return ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+}
 
 // One dense layer for a (row group, batch tile) item.  R consecutive output
 // rows share every load of the inputs (R > 1 when several requests are
@@ -300,8 +308,7 @@ __device__ __forceinline__ void sum_parts(const float* base, const float* parts,
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           const int w = w0 + i * G;
-          v[i] = w < nparts ? *reinterpret_cast<const float4*>(parts + (int64_t)w * n + 4 * c)
-                            : make_float4(0.f, 0.f, 0.f, 0.f);
+          v[i] = load4_or_zero(parts + (int64_t)w * n + 4 * c, parts, w < nparts);
         }
 #pragma unroll
         for (int i = 0; i < 8; ++i) acc = make_float4(acc.x + v[i].x, acc.y + v[i].y, acc.z + v[i].z, acc.w + v[i].w);
@@ -451,16 +458,15 @@ __global__ __launch_bounds__(256) void gate_split_block_kernel(SplitArgs p) {
   for (int c = 0; c < KC; ++c) {
     const int k = c * 256 + 4 * lane;
     const bool in = k < p.dt;
-    gk[c] = in ? *reinterpret_cast<const float4*>(p.gain + k) : zero;
+    gk[c] = load4_or_zero(p.gain + k, p.gain, in);
 #pragma unroll
     for (int jj = 0; jj < HW; ++jj) {
-      wg[jj][c] = in ? *reinterpret_cast<const float4*>(p.Wg + (int64_t)(j0 + jj) * p.dt + k) : zero;
-      wu[jj][c] = in ? *reinterpret_cast<const float4*>(p.Wu + (int64_t)(j0 + jj) * p.dt + k) : zero;
+      wg[jj][c] = load4_or_zero(p.Wg + (int64_t)(j0 + jj) * p.dt + k, p.Wg, in);
+      wu[jj][c] = load4_or_zero(p.Wu + (int64_t)(j0 + jj) * p.dt + k, p.Wu, in);
     }
     const int r = threadIdx.x + 256 * c;
 #pragma unroll
-    for (int q = 0; q < HW; ++q)
-      wd[c][q] = r < p.dt ? *reinterpret_cast<const float4*>(p.Wd + (int64_t)r * 2 * p.dt + jb + 4 * q) : zero;
+    for (int q = 0; q < HW; ++q) wd[c][q] = load4_or_zero(p.Wd + (int64_t)r * 2 * p.dt + jb + 4 * q, p.Wd, r < p.dt);
   }
   // the block input for every request: the residual plus the previous block's partial sums
   sum_parts<256>(p.z_base, p.parts_in, p.nparts_in, n, sz, sscratch);
