@@ -27,8 +27,12 @@
  *     returns a negative status and enqueues nothing.  oda_last_error() then
  *     holds a thread-local description.
  *   - All work is enqueued on `stream` (NULL = the default stream).
- *   - Device-data contract (not checked): seq_lens[b] in [1, max_seq_len];
- *     every block-table entry a request uses is in [0, num_blocks).
+ *   - Device-data contract: seq_lens[b] in [1, max_seq_len]; every block-table
+ *     entry a request uses in [0, num_blocks); listed requests in [0, batch).
+ *     The kernels check it and never address memory with a value outside it:
+ *     attention writes NaN rows (out and lse) for a request whose length or
+ *     used table entry is out of range, the commit writes nothing for it, and
+ *     listed requests outside the batch are skipped.
  *   - The library keeps no state between calls.  Workspaces may be reused by
  *     later calls on the same stream; calls that share a workspace must not
  *     overlap in time.

@@ -90,6 +90,11 @@ struct AttnArgs {
   int32_t nvb_max;          // host bound on visited blocks per request
   int32_t select;
   float scale_log2;         // scale * log2(e)
+  // device-data checks: a length outside [1, max_len], a block-table entry
+  // outside [0, num_blocks) or a listed request outside [0, B) is never used
+  // to address memory; the affected outputs become NaN (or are skipped)
+  int32_t max_len;
+  int64_t num_blocks;
 };
 
 // Positions of one request attended through the cache, as block ranges.
@@ -141,7 +146,7 @@ __device__ __forceinline__ bool resolve_request(const AttnArgs& a, int slot, int
   if (a.select == kSelList) {
     if (slot >= a.n_work[0]) return false;
     b = a.work_list[slot];
-    return true;
+    return b >= 0 && b < a.B;
   }
   b = slot;
   if (a.select == kSelFlags) return a.flags[slot] != 0;
@@ -229,13 +234,21 @@ struct Run {
   const uint16_t* vbase;
   const int32_t* bt;
   int64_t blk_stride;
+  int64_t nblocks;
   int v_lo, v_hi;
 };
 
-__device__ __forceinline__ int table_chunk(const Run& r, int chunk, int lane) {
+// Physical blocks of 64 consecutive virtual blocks, one per lane.  An entry
+// outside [0, num_blocks) reads block 0 instead and sets `bad`.
+__device__ __forceinline__ int table_chunk(const Run& r, int chunk, int lane, int& bad) {
   const int v = r.v_lo + chunk * 64 + lane;
-  return v < r.v_hi ? r.bt[logical_block(r.geo, v)] : 0;
+  const int e = v < r.v_hi ? r.bt[logical_block(r.geo, v)] : 0;
+  const bool ok = e >= 0 && e < r.nblocks;
+  bad |= ok ? 0 : 1;
+  return ok ? e : 0;
 }
+
+__device__ __forceinline__ bool valid_len(const AttnArgs& a, int n) { return n >= 1 && n <= a.max_len; }
 
 template <int D>
 __device__ __forceinline__ void load_pair(PairTile<D>& t, const Run& r, int v, int tbl, int lane) {
@@ -385,13 +398,23 @@ void attn_split_kernel(AttnArgs a) {
   if (!resolve_request(a, slot, b)) return;
   b = uniform(b);
   const int n = uniform(a.seq_lens[b]);
+  const int G = a.G;
+  if (!valid_len(a, n)) {   // no history is addressed: the request's rows become NaN
+    if (split == 0) {
+      const int64_t q0 = (((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G) * D;
+      for (int e = threadIdx.x; e < G * D; e += kWaves * 64) {
+        a.out[q0 + e] = __builtin_nanf("");
+        if (e % D == 0 && a.lse != nullptr) a.lse[((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G + e / D] = __builtin_nanf("");
+      }
+    }
+    return;
+  }
   Run r;
   r.geo = geometry(n, kLocal ? a.n_sink : 0, a.window, a.has_cur);
   const int bps = effective_bps(a);
   // (nvb = 0 happens only with the candidate as the sole position: one item, no blocks)
   const int nsplit = max(1, (r.geo.nvb + bps - 1) / bps);
   if (split >= nsplit) return;   // uniform over the workgroup: no barrier is skipped by part of it
-  const int G = a.G;
 
   // this wavefront's run: a contiguous share of the split's pairs
   const int v_begin = split * bps;
@@ -405,6 +428,7 @@ void attn_split_kernel(AttnArgs a) {
   r.kbase = a.k_cache + (int64_t)l * a.kv_layer_stride + (int64_t)g * head_elems;
   r.vbase = a.v_cache + (int64_t)l * a.kv_layer_stride + (int64_t)g * head_elems;
   r.blk_stride = (int64_t)a.Hkv * head_elems;
+  r.nblocks = a.num_blocks;
   r.bt = a.block_table + (int64_t)b * a.MB;
 
   f32x4 o[NT];
@@ -420,8 +444,9 @@ void attn_split_kernel(AttnArgs a) {
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) qf[kk] = (h16 < G) ? load16(qrow + 32 * kk + 8 * j) : bf16x8{};
 
-    int tbl = table_chunk(r, 0, lane);
-    int tbl_next = table_chunk(r, 1, lane);
+    int bad = 0;
+    int tbl = table_chunk(r, 0, lane, bad);
+    int tbl_next = table_chunk(r, 1, lane, bad);
 #if ODA_SPLIT_PREFETCH
     PairTile<D> ta, tb;
     load_pair<D>(ta, r, r.v_lo, tbl, lane);
@@ -430,7 +455,7 @@ void attn_split_kernel(AttnArgs a) {
       if (more1) {
         if (((v + 2 - r.v_lo) & 63) == 0) {   // entering the next 64-block chunk of the table
           tbl = tbl_next;
-          tbl_next = table_chunk(r, ((v + 2 - r.v_lo) >> 6) + 1, lane);
+          tbl_next = table_chunk(r, ((v + 2 - r.v_lo) >> 6) + 1, lane, bad);
         }
         load_pair<D>(tb, r, v + 2, tbl, lane);
       }
@@ -439,7 +464,7 @@ void attn_split_kernel(AttnArgs a) {
       if (v + 4 < r.v_hi) {
         if (((v + 4 - r.v_lo) & 63) == 0) {
           tbl = tbl_next;
-          tbl_next = table_chunk(r, ((v + 4 - r.v_lo) >> 6) + 1, lane);
+          tbl_next = table_chunk(r, ((v + 4 - r.v_lo) >> 6) + 1, lane, bad);
         }
         load_pair<D>(ta, r, v + 4, tbl, lane);
       }
@@ -449,7 +474,7 @@ void attn_split_kernel(AttnArgs a) {
     for (int v = r.v_lo; v < r.v_hi; v += 2) {
       if (v > r.v_lo && ((v - r.v_lo) & 63) == 0) {
         tbl = tbl_next;
-        tbl_next = table_chunk(r, ((v - r.v_lo) >> 6) + 1, lane);
+        tbl_next = table_chunk(r, ((v - r.v_lo) >> 6) + 1, lane, bad);
       }
       PairTile<D> ta;
       load_pair<D>(ta, r, v, tbl, lane);
@@ -458,6 +483,10 @@ void attn_split_kernel(AttnArgs a) {
 #endif
     l_run += __shfl_xor(l_run, 16);
     l_run += __shfl_xor(l_run, 32);
+    if (__any(bad)) {   // a block-table entry out of range: this request's rows become NaN
+      m_run = __builtin_nanf("");
+      l_run = __builtin_nanf("");
+    }
   }
 
   // combine the wavefronts through LDS
@@ -548,6 +577,7 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(AttnArgs a) {
   if (!resolve_request(a, slot, b)) return;
   b = uniform(b);
   const int n = uniform(a.seq_lens[b]);
+  if (!valid_len(a, n)) return;   // the split kernel wrote NaN rows
   const Geometry geo = geometry(n, a.n_sink, a.window, a.has_cur);
   const int bps = effective_bps(a);
   const int nsplit = max(1, (geo.nvb + bps - 1) / bps);
@@ -737,6 +767,8 @@ oda_status run_attention(const oda_attn_shape* s, const oda_attn_inputs* in, boo
   a.part_o = static_cast<float*>(ws);
   a.part_ml = plan.bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + plan.off_ml) : nullptr;
   a.kv_layer_stride = s->num_blocks * s->num_kv_heads * kBlock * s->head_dim;
+  a.max_len = s->max_seq_len;
+  a.num_blocks = s->num_blocks;
   a.L = s->num_layers;
   a.B = s->batch;
   a.Hq = s->num_q_heads;

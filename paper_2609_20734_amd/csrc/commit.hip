@@ -25,6 +25,7 @@ struct CommitArgs {
   const uint16_t* v_full;
   const int32_t* flags;
   int64_t kv_layer_stride;   // elements between layers of the caches
+  int64_t NB;                // physical blocks
   int32_t L, B, Hkv, D, MB;
   int32_t advance;
 };
@@ -42,10 +43,13 @@ __global__ __launch_bounds__(kThreads) void commit_copy_kernel(CommitArgs a) {
   const int d8 = threadIdx.x;
   if (d8 >= a.D / 8) return;
   const int pos = a.seq_lens[b] - 1;
+  // a length or block-table entry outside the cache writes nothing
+  if (pos < 0 || pos >= a.MB * kBlock) return;
+  const int64_t blk = a.block_table[(int64_t)b * a.MB + pos / kBlock];
+  if (blk < 0 || blk >= a.NB) return;
   const bool full = a.flags != nullptr && a.flags[b] != 0;
   const uint16_t* ks = full ? a.k_full : a.k_local;
   const uint16_t* vs = full ? a.v_full : a.v_local;
-  const int64_t blk = a.block_table[(int64_t)b * a.MB + pos / kBlock];
   const int slot = pos % kBlock;
   const int64_t src = (((int64_t)l * a.B + b) * a.Hkv + g) * a.D + d8 * 8;
   const int64_t dst = (int64_t)l * a.kv_layer_stride + (blk * a.Hkv + g) * kBlock * a.D;
@@ -99,6 +103,7 @@ extern "C" oda_status oda_commit_kv(const oda_attn_shape* shape, uint16_t* k_cac
   a.Hkv = shape->num_kv_heads;
   a.D = shape->head_dim;
   a.MB = shape->max_blocks_per_seq;
+  a.NB = shape->num_blocks;
   a.advance = advance != 0;
   (void)hipGetLastError();
   const int64_t units = (int64_t)shape->batch * shape->num_layers * shape->num_kv_heads;

@@ -96,7 +96,10 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs p) {
   const int count = selected_count(p.n_work, p.B);
   if (s0 >= count) return;
   const int nb = min(T, count - s0);
-  const int my_req = lane < nb ? selected_request(p.work_list, s0 + lane) : 0;
+  // a listed request outside [0, B) is computed as request 0 and not stored
+  const int listed = lane < nb ? selected_request(p.work_list, s0 + lane) : 0;
+  const bool my_ok = listed >= 0 && listed < p.B;
+  const int my_req = my_ok ? listed : 0;
   int req[T];
 #pragma unroll
   for (int bi = 0; bi < T; ++bi) req[bi] = __shfl(my_req, bi);
@@ -188,8 +191,9 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs p) {
     }
   }
   const int j = lane / T, bi = lane % T;
-  if (lane >= kAcc || bi >= nb) return;
-  const int b = selected_request(p.work_list, s0 + bi);
+  const bool ok = __shfl(my_ok ? 1 : 0, bi) != 0;
+  if (lane >= kAcc || bi >= nb || !ok) return;
+  const int b = selected_request(p.work_list, s0 + bi);   // in [0, B): checked above
   const int row = row0 + j;
   const float inv = norm ? rsqrtf(my_ss / (float)p.K + p.eps) : 1.f;
   float out;
@@ -232,6 +236,7 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(RopeArgs p) {
   const int h = (blockIdx.x % p.heads_per_group) * kWaves + wave;
   if (slot >= selected_count(p.n_work, p.B) || h >= heads) return;
   const int b = selected_request(p.work_list, slot);
+  if (b < 0 || b >= p.B) return;   // a listed request outside the batch is skipped
   const int half = p.D / 2;
   if (lane >= half) return;
   const float* src = p.qkv + ((int64_t)b * heads + h) * p.D;
@@ -297,7 +302,9 @@ __global__ __launch_bounds__(256) void copy_rows_kernel(const float* src, float*
                                                        const int32_t* work_list, const int32_t* n_work) {
   const int slot = blockIdx.x;
   if (slot >= selected_count(n_work, B)) return;
-  const int64_t base = (int64_t)selected_request(work_list, slot) * row_len;
+  const int b = selected_request(work_list, slot);
+  if (b < 0 || b >= B) return;   // a listed request outside the batch is skipped
+  const int64_t base = (int64_t)b * row_len;
   for (int k = threadIdx.x * 4; k < row_len; k += 256 * 4)
     *reinterpret_cast<float4*>(dst + base + k) = *reinterpret_cast<const float4*>(src + base + k);
 }
