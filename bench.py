@@ -5,19 +5,27 @@ A step is one pass of the whole path over one batch: Local decode attention
 for every layer and request, the recall gate (score + device predicate +
 compaction), and Full decode attention for the flagged requests only, all on
 one stream.  The recall rate rho is swept by the threshold tau (calibrated on
-the gate's scores over the K timed steps), and compared against the
-always-Full baseline (Full for every request, no Local, no gate).
+the gate's scores over the K timed steps) or, for the mixed-length batch, by
+Bernoulli schedules of forced flags (threshold-driven rates reported beside
+them), and compared against the always-Full baseline (Full for every request,
+no Local, no gate).
 
 Timing: every step is bracketed by HIP events on the stream the library
 launches on.  Headline ("cold") numbers read a 1 GiB scratch buffer between
 steps, outside the events, so the 256 MB Infinity Cache holds no KV or gate
-weights at the start of a step; "warm" numbers run the K steps back to back.
+weights at the start of a step; each operating point runs `reps` repetitions
+of K steps and reports the median of the repetitions' means (with their min
+and max); "warm" numbers run the K steps back to back.  Two launch modes:
+stacked (one call covers every layer of a group; the metric) and per-layer
+(one call per layer, eager and as a captured HIP graph; the realism check).
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config llama3-8b] [--head paper|mlp]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--reps R] [--config llama3-8b] [--head paper|mlp]
 
 Prints one JSON line: the headline value (µs per step at the recall rate
-nearest 0.1), the per-rate sweep for both recall heads, the decode loop, the
-roofline of the dominant kernel and the CPU oracle baseline.
+nearest 0.1), the per-rate sweep for both recall heads, the per-layer launch
+mode, the decode loop, Local with and without sinks, the streaming-read
+ceiling, the roofline of the dominant kernel and the CPU oracle baseline (one
+thread and a process pool, timed before the GPU is touched).
 
     python bench.py --decoder [--lengths 4139,15918,...]
 
@@ -117,10 +125,7 @@ class Bench:
         dev = torch.device("cuda:0")
         self.dev = dev
         B = wl.batch
-        if wl.seq_lens:
-            seq = np.array(wl.seq_lens, dtype=np.int32)
-        else:
-            seq = S.uniform_seq_lens(seed, B, *wl.seq_range)
+        seq = workload_seq_lens(wl, seed)
         self.seq_host = seq
         self.growth = growth     # positions a decode loop may append (blocks reserved in the table)
         mb = int(math.ceil((seq.max() + growth) / 16))
@@ -145,6 +150,12 @@ class Bench:
         self.work = torch.zeros(B, dtype=torch.int32, device=dev)
         self.n_work = torch.zeros(1, dtype=torch.int32, device=dev)
         self.counter = torch.zeros(1, dtype=torch.int64, device=dev)
+        # staging copies of one step's gate inputs and forced flags (per-layer launch mode)
+        self.h_stage = torch.zeros((B, wl.d_model), dtype=torch.float32, device=dev)
+        self.e_stage = torch.zeros_like(self.h_stage)
+        self.l_stage = torch.zeros_like(self.h_stage)
+        self.f_stage = torch.zeros(B, dtype=torch.int32, device=dev)
+        self.sink = torch.zeros(64, dtype=torch.int32, device=dev)
         # 1 GiB read between steps evicts the 256 MB Infinity Cache with clean lines
         # (a write flush would leave dirty lines for the next step to write back)
         self.flush_buf = torch.ones(1 << 28, dtype=torch.float32, device=dev)
@@ -166,12 +177,14 @@ class Bench:
         self.ws_gate = torch.empty(P.gate_workspace_size(self.gate, wl.batch), dtype=torch.uint8, device=self.dev)
 
     # -- calls ---------------------------------------------------------------
-    def step_calls(self, tau, forced=None):
-        """Per step t: the list of pre-marshalled calls of one decode step."""
+    def step_calls(self, tau, forced=None, gated_only=False):
+        """Per step t: the list of pre-marshalled calls of one decode step.
+        gated_only: the Full retry covers only the gated layer groups (natively
+        windowed layers keep their Local result, which is already native)."""
         P = self.P
         local = [P.prepare_local(s.shape, s.inp, *s.local_args, s.out, s.lse, s.ws_local) for s in self.stacks]
         full = [P.prepare_full(s.shape, s.inp, s.stack.native_window, None, self.work, self.n_work, s.out, s.lse,
-                               s.ws_full) for s in self.stacks]
+                               s.ws_full) for s in self.stacks if s.stack.gated or not gated_only]
         steps = []
         for t in range(self.K):
             fo = None if forced is None else forced[t]
@@ -277,9 +290,14 @@ class Bench:
         return out
 
     # -- timing --------------------------------------------------------------
-    def timed(self, steps, warmup, cold=True):
+    def timed(self, steps, warmup, cold=True, pre=None):
+        """Time each of the K call lists in `steps` (one decode step each)
+        between HIP events; pre(t), if given, runs before step t's start event
+        (after the cache flush)."""
         torch = self.torch
         for t in range(warmup):
+            if pre is not None:
+                pre(t % len(steps))
             for c in steps[t % len(steps)]:
                 c()
         torch.cuda.synchronize()
@@ -293,6 +311,8 @@ class Bench:
         for t in range(K):
             if cold:
                 self.flush()
+            if pre is not None:
+                pre(t)
             evs[t][0].record()
             for c in steps[t]:
                 c()
@@ -324,6 +344,104 @@ class Bench:
                                      st.out, st.lse, st.ws_local) for st in self.stacks]
             res[f"{name}_us"] = self.kernel_time(calls, reps, cold=True)
         return res
+
+    # -- per-layer launch mode --------------------------------------------------
+    def _layer_state(self):
+        """One-layer shapes, per-layer inputs and workspaces (built once)."""
+        if getattr(self, "_layers", None) is None:
+            torch, P = self.torch, self.P
+            scale = 1.0 / math.sqrt(self.wl.head_dim)
+            self._layers = []
+            for st in self.stacks:
+                s = st.shape
+                sh = P.Shape(1, s.batch, s.num_q_heads, s.num_kv_heads, s.head_dim, s.max_blocks_per_seq,
+                             s.max_seq_len, s.num_blocks, s.split_blocks)
+                ws_l = torch.empty(max(256, P.attn_workspace_size(sh, *st.local_args)), dtype=torch.uint8,
+                                   device=self.dev)
+                ws_f = torch.empty(max(256, P.attn_workspace_size(sh, 0, st.stack.native_window)),
+                                   dtype=torch.uint8, device=self.dev)
+                ins = [P.inputs(st.q[l], st.k[l], st.v[l], self.dtable, self.dseq, scale)
+                       for l in range(st.stack.num_layers)]
+                self._layers.append((st, sh, ws_l, ws_f, ins))
+        return self._layers
+
+    def per_layer_calls(self, tau, forced):
+        """One decode step as one call per layer: every layer's Local, the gate
+        (reading the staged inputs), every layer's Full over the compacted list."""
+        P = self.P
+        calls = []
+        for st, sh, ws_l, _, ins in self._layer_state():
+            calls += [P.prepare_local(sh, inp, *st.local_args, st.out[l], st.lse[l], ws_l)
+                      for l, inp in enumerate(ins)]
+        calls.append(P.prepare_gate(self.gate, self.wl.batch, self.h_stage, self.e_stage, self.l_stage, tau,
+                                    self.f_stage if forced is not None else None, self.score, self.flags,
+                                    self.work, self.n_work, self.counter, self.ws_gate))
+        for st, sh, _, ws_f, ins in self._layer_state():
+            calls += [P.prepare_full(sh, inp, st.stack.native_window, None, self.work, self.n_work, st.out[l],
+                                     st.lse[l], ws_f) for l, inp in enumerate(ins)]
+        return calls
+
+    def per_layer(self, tau, forced, warmup):
+        """Per-layer launches of the K steps, eager and replayed as one captured
+        HIP graph per step shape (gate inputs staged before each step, outside
+        the events).  Returns (eager, graph) timing dicts."""
+        torch = self.torch
+        K = self.K
+
+        def pre(t):
+            self.h_stage.copy_(self.h[t])
+            self.e_stage.copy_(self.e[t])
+            self.l_stage.copy_(self.l[t])
+            if forced is not None:
+                self.f_stage.copy_(forced[t])
+
+        calls = self.per_layer_calls(tau, forced)
+        eager = self.timed([calls] * K, warmup, cold=True, pre=pre)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for c in self.per_layer_calls(tau, forced):     # prepared on the capture stream
+                c()
+        graph = self.timed([[g.replay]] * K, warmup, cold=True, pre=pre)
+        del g
+        return eager, graph
+
+    # -- single measurements -------------------------------------------------------
+    def local_sinks(self, reps=20):
+        """Local alone (every layer group, cold) with the configured sinks and
+        with s = 0 (window only)."""
+        torch, P = self.torch, self.P
+        res = {}
+        for name, zero in (("sinks", False), ("no_sinks", True)):
+            calls = []
+            for st in self.stacks:
+                s_, w_ = st.local_args
+                if zero:
+                    s_ = 0
+                ws = torch.empty(max(256, P.attn_workspace_size(st.shape, s_, w_)), dtype=torch.uint8,
+                                 device=self.dev)
+                calls.append(P.prepare_local(st.shape, st.inp, s_, w_, st.out, st.lse, ws))
+            res[f"{name}_us"] = self.kernel_time(calls, reps, cold=True)
+        res["n_sink"] = max(st.local_args[0] for st in self.stacks)
+        return res
+
+    def read_ceiling(self, nbytes, reps=10):
+        """Streaming-read ceiling: oda_stream_read over the first nbytes of the
+        KV caches (cold), in GB/s."""
+        torch, P = self.torch, self.P
+        spans = []
+        left = nbytes
+        for st in self.stacks:
+            for t in (st.k, st.v):
+                take = min(left, t.numel() * t.element_size())
+                take -= take % 16
+                if take > 0:
+                    spans.append((t, take))
+                    left -= take
+        calls = [P.prepare_stream_read(t, n, self.sink) for t, n in spans]
+        done = nbytes - left
+        us = self.kernel_time(calls, reps, cold=True)
+        return dict(bytes=done, us=us, GBps=done / us / 1e3)
 
     def kernel_time(self, calls, reps, cold=True):
         """Mean duration (us) of one call bracketed by events on its stream."""
@@ -360,8 +478,9 @@ def taus_for(scores, rhos):
     return out
 
 
-def bytes_for(wl, seq, flagged_frac_per_step, head):
-    """Average algorithmic bytes per step given the realised per-step flag sets."""
+def bytes_for(wl, seq, flagged_frac_per_step, head, gated_only=False):
+    """Algorithmic bytes of one step: (Local, gate, per-request Full retry);
+    gated_only restricts the retry to the gated layer groups."""
     from paper_2609_20734_amd import ledger as LG
     B = wl.batch
     local = sum(LG.attention_bytes(seq, *(st.local_sink, st.local_window) if st.gated else (0, st.native_window),
@@ -369,101 +488,247 @@ def bytes_for(wl, seq, flagged_frac_per_step, head):
                 for st in wl.stacks)
     gate = LG.gate_bytes(head, B, wl.d_model, wl.d_hidden)["total"]
     full_all = [sum(LG.attention_bytes(seq, 0, st.native_window, st.num_layers, wl.num_q_heads, wl.num_kv_heads,
-                                       wl.head_dim, requests=[b])["total"] for st in wl.stacks) for b in range(B)]
+                                       wl.head_dim, requests=[b])["total"] for st in wl.stacks
+                    if st.gated or not gated_only) for b in range(B)]
     return local, gate, full_all
 
 
-def cpu_baseline(b, rho, budget_s=15.0):
-    """The fp64 oracle timed on a bounded sample of the same step, 1 thread."""
+# Host-side state of the CPU baseline, set before its process pool forks (the
+# workers read it copy-on-write).
+_CPU = {}
+
+
+def _cpu_layer(i):
+    """K and V of distinct cache layer i (a seeded N(0,1) bf16 slab tiled to
+    the cache size: the oracle's work does not depend on the values)."""
+    import oda_synth as S
+    c = _CPU
+    while len(c["k"]) <= i:
+        j = len(c["k"])
+        ks, vs = S.kv_cache_shapes(1, c["nb"], c["Hkv"], c["D"])
+        slab_k = S.normal_bf16(S.rng(c["seed"] + j, S.STREAM_K), (1 << 20,))
+        slab_v = S.normal_bf16(S.rng(c["seed"] + j, S.STREAM_V), (1 << 20,))
+        c["k"].append(np.resize(slab_k, ks))
+        c["v"].append(np.resize(slab_v, vs))
+    return c["k"][i], c["v"][i]
+
+
+def _cpu_task(task, branch):
+    """Oracle time (s) of one (stack, layer, request) slice, Local or Full."""
+    from oracle import attention as OA
+    c = _CPU
+    si, l, b = task
+    s_, w_, native = c["stacks"][si]
+    k, v = _cpu_layer(l % c["distinct"])
+    if branch == "local":
+        pos = (lambda n: OA.local_set(n, s_, w_)) if w_ > 0 else (lambda n: OA.native_window_set(n, native))
+    else:
+        pos = lambda n: OA.native_window_set(n, native)
+    t0 = time.perf_counter()
+    OA.decode_attention(c["q"][si][l:l + 1], k, v, c["table"], c["seq"], pos, c["scale"], requests=[b])
+    return time.perf_counter() - t0
+
+
+def _cpu_worker_init():
+    from threadpoolctl import threadpool_limits
+    _CPU["limits"] = threadpool_limits(limits=1)
+
+
+def _cpu_local_task(task):
+    return _cpu_task(task, "local")
+
+
+def _cpu_full_task(task):
+    return _cpu_task(task, "full")
+
+
+def workload_seq_lens(wl, seed):
+    import oda_synth as S
+    if wl.seq_lens:
+        return np.array(wl.seq_lens, dtype=np.int32)
+    return S.uniform_seq_lens(seed, wl.batch, *wl.seq_range)
+
+
+def cpu_baseline(wl, head, seed, rho, budget_s=10.0, mem_cap=8e9):
+    """The fp64 oracle timed on the host on a bounded sample of the step, in
+    two modes: (i) one thread (BLAS and OpenMP limited to 1) running the
+    slices in turn; (ii) a process pool over (layer, request) slices, one
+    single-threaded worker per core this process may use (at most 16).  Runs
+    before the GPU is touched, so the pool's fork copies no GPU state.  Each
+    slice is Local (or, for natively windowed layers, their window) or Full of
+    one request in one layer; times are extrapolated to the whole step in
+    attended positions, and the step weighs Full by rho (plus one gate
+    evaluation for the batch)."""
+    import multiprocessing as mp
+
     from threadpoolctl import threadpool_limits
 
+    import oda_synth as S
     from oracle import attention as OA
     from oracle import gate as OG
-    wl = b.wl
-    st = b.stacks[-1]
-    L = st.stack.num_layers
-    seq = b.seq_host
+    B, D, Hkv = wl.batch, wl.head_dim, wl.num_kv_heads
+    seq = workload_seq_lens(wl, seed)
+    mb = int(math.ceil(seq.max() / 16))
+    table, nb = S.paged_block_table(S.rng(seed, S.STREAM_TABLE), seq, mb, permute=wl.permute)
+    layer_bytes = 2 * nb * Hkv * D * 16 * 2
+    _CPU.clear()
+    _CPU.update(seed=seed, nb=nb, Hkv=Hkv, D=D, k=[], v=[], table=table, seq=seq, scale=1.0 / math.sqrt(D),
+                distinct=max(1, min(sum(st.num_layers for st in wl.stacks), int(mem_cap // layer_bytes))),
+                q=[S.normal_bf16(S.rng(seed + len(st.name), S.STREAM_Q), (st.num_layers, B, wl.num_q_heads, D))
+                   for st in wl.stacks],
+                stacks=[(st.local_sink if st.gated else 0, st.local_window if st.gated else 0, st.native_window)
+                        for st in wl.stacks])
+    tasks = [(si, l, b) for si, st in enumerate(wl.stacks) for l in range(st.num_layers) for b in range(B)]
+
+    def positions(task, branch):
+        si, _, b = task
+        s_, w_, native = _CPU["stacks"][si]
+        n = int(seq[b])
+        if branch == "local" and w_ > 0:
+            return len(OA.local_set(n, s_, w_))
+        return len(OA.native_window_set(n, native))
+
+    tot_local = sum(positions(t, "local") for t in tasks)
+    tot_full = sum(positions(t, "full") for t in tasks)
     with threadpool_limits(limits=1):
-        # gate (one step)
+        params = S.gate_params(seed, head, wl.d_model, wl.d_hidden)
+        h, e, l_ = (x[0].astype(np.float64) for x in S.gate_inputs(seed, 1, B, wl.d_model))
         t0 = time.perf_counter()
-        params = b.params.cpu().numpy()
-        h, e, l = (x[0].cpu().numpy().astype(np.float64) for x in (b.h, b.e, b.l))
-        if b.head == "paper":
-            OG.paper_head_score(params, wl.d_model, wl.d_hidden, 1e-6, h, e, l)
+        if head == "paper":
+            OG.paper_head_score(params, wl.d_model, wl.d_hidden, 1e-6, h, e, l_)
         else:
-            OG.mlp_score(params, wl.d_model, wl.d_hidden, l)
+            OG.mlp_score(params, wl.d_model, wl.d_hidden, l_)
         t_gate = time.perf_counter() - t0
-        # per layer: copy the layer's cache once, then Local and Full for every request
-        q_all = b.stacks[-1].q.cpu().numpy().view(np.uint16)
-        table = b.dtable.cpu().numpy()
-        t_local = t_full = 0.0
-        layers = 0
-        for layer in range(L):
-            kl = st.k[layer:layer + 1].cpu().view(b.torch.int16).numpy().view(np.uint16)
-            vl = st.v[layer:layer + 1].cpu().view(b.torch.int16).numpy().view(np.uint16)
-            ql = q_all[layer:layer + 1]
-            s_, w_ = st.local_args
-            t0 = time.perf_counter()
-            OA.decode_attention(ql, kl, vl, table, seq, lambda n: OA.local_set(n, s_, w_), 1 / math.sqrt(wl.head_dim))
-            t1 = time.perf_counter()
-            OA.decode_attention(ql, kl, vl, table, seq, lambda n: OA.native_window_set(n, st.stack.native_window),
-                                1 / math.sqrt(wl.head_dim))
-            t2 = time.perf_counter()
-            t_local += t1 - t0
-            t_full += t2 - t1
-            layers += 1
-            if t_local + t_full + t_gate > budget_s:
+        # (i) one thread
+        t_loc = t_full = 0.0
+        done = 0
+        for t in tasks:
+            _cpu_layer(t[1] % _CPU["distinct"])
+            t_loc += _cpu_task(t, "local")
+            t_full += _cpu_task(t, "full")
+            done += 1
+            if t_loc + t_full >= budget_s:
                 break
-    scale = wl.num_layers / layers
-    per_step = t_gate + scale * (t_local + rho * t_full)
-    return dict(value=per_step * 1e6, unit="us/step", cores=1, kind="oracle",
-                sample=f"{layers} of {wl.num_layers} layers (Local + Full, all {wl.batch} requests) and one gate "
-                       f"evaluation, fp64 NumPy, 1 thread; extrapolated linearly to {wl.num_layers} layers at "
-                       f"rho={rho} (Full time weighted by rho)",
-                measured_s=t_gate + t_local + t_full)
+    s_loc = sum(positions(t, "local") for t in tasks[:done])
+    s_full = sum(positions(t, "full") for t in tasks[:done])
+    one = t_gate + t_loc * tot_local / s_loc + rho * t_full * tot_full / s_full
+    # (ii) process pool over (layer, request)
+    cores = min(16, len(os.sched_getaffinity(0)))
+    per_task = (t_loc + t_full) / done
+    m = min(len(tasks), cores * max(1, int(budget_s / max(per_task, 1e-6))))
+    for t in tasks[:m]:
+        _cpu_layer(t[1] % _CPU["distinct"])
+    ctx = mp.get_context("fork")
+    with ctx.Pool(cores, initializer=_cpu_worker_init) as pool:
+        pool.map(_cpu_local_task, tasks[:min(m, cores)])         # first touch of the workers
+        t0 = time.perf_counter()
+        pool.map(_cpu_local_task, tasks[:m], chunksize=1)
+        w_loc = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        pool.map(_cpu_full_task, tasks[:m], chunksize=1)
+        w_full = time.perf_counter() - t0
+    p_loc = sum(positions(t, "local") for t in tasks[:m])
+    p_full = sum(positions(t, "full") for t in tasks[:m])
+    pooled = t_gate + w_loc * tot_local / p_loc + rho * w_full * tot_full / p_full
+    _CPU.clear()
+    note = (f"K/V: seeded N(0,1) bf16 slabs tiled to the cache shape, {wl.batch} request(s), block table and "
+            f"lengths as on the GPU; rho={rho} weighs Full; one gate evaluation ({head} head) for the batch")
+    return dict(value=one * 1e6, unit="us/step", cores=1, kind="oracle",
+                sample=f"{done} of {len(tasks)} (layer, request) slices, Local + Full, fp64 NumPy, 1 thread"
+                       + (", extrapolated to every slice in attended positions" if done < len(tasks) else "")
+                       + "; " + note,
+                measured_s=t_gate + t_loc + t_full,
+                host_cpus=os.cpu_count(), affinity_cpus=len(os.sched_getaffinity(0)),
+                pool=dict(value=pooled * 1e6, unit="us/step", cores=cores, kind="oracle",
+                          sample=f"{m} of {len(tasks)} slices over a {cores}-process pool (one thread each), "
+                                 f"wall clock" + (", extrapolated to every slice in attended positions"
+                                                  if m < len(tasks) else ""),
+                          measured_s=w_loc + w_full))
 
 
-def run_sweep(b, wl, args, full_us):
-    """Time the step over the configuration's recall rates (threshold-driven) or
-    Bernoulli schedules (forced flags, gate still run); one entry per point."""
+def sweep_points(b, wl, args):
+    """The configuration's operating points: recall rates set by the threshold
+    (calibrated on this head's scores over the K steps) and Bernoulli schedules
+    of forced flags (the gate still runs and is timed)."""
     import torch
-    K = b.K
-    local_b, gate_b, full_b = bytes_for(wl, b.seq_host, None, b.head)
-    bytes_full = sum(full_b)
-    sweep = []
+
+    import oda_synth as S
+    pts = []
     if wl.rhos:
-        sc = b.scores()
-        taus = taus_for(sc, wl.rhos)
-        points = [(rho, taus[rho], None, None) for rho in wl.rhos]
+        taus = taus_for(b.scores(), wl.rhos)
+        pts += [dict(mode="tau", rho=r, tau=taus[r], forced=None, forced_np=None) for r in wl.rhos]
+    for p in wl.bernoulli:
+        f = S.bernoulli_flags(args.seed, b.K, wl.batch, p)
+        pts.append(dict(mode="bernoulli", rho=p, tau=0.0, forced=torch.from_numpy(f).to(b.dev), forced_np=f))
+    return pts
+
+
+def primary_mode(wl):
+    return "bernoulli" if wl.bernoulli else "tau"
+
+
+def step_bytes(wl, b, pt, recalled, gated_only=False):
+    local_b, gate_b, full_b = bytes_for(wl, b.seq_host, None, b.head, gated_only)
+    _, _, full_all = bytes_for(wl, b.seq_host, None, b.head)
+    K = b.K
+    if pt["forced_np"] is None:
+        full_part = recalled / (K * wl.batch) * sum(full_b)
     else:
-        import oda_synth as S
-        points = []
-        for p in wl.bernoulli:
-            forced_np = S.bernoulli_flags(args.seed, K, wl.batch, p)
-            points.append((p, 0.0, torch.from_numpy(forced_np).to(b.dev), forced_np))
-    for rho, tau, forced, forced_np in points:
-        r = b.timed(b.step_calls(tau, forced=forced), args.warmup, cold=True)
-        real = r["recalled"] / (K * wl.batch)
-        if forced_np is None:
-            full_part = real * bytes_full
-        else:
-            full_part = float(np.mean([(forced_np[t] * np.array(full_b)).sum() for t in range(K)]))
-        step_bytes = local_b + gate_b + full_part
-        ent = dict(rho=rho, realised_rho=real, us=r["us_mean"], us_median=r["us_median"], us_min=r["us_min"],
-                   us_max=r["us_max"], GBps=step_bytes / r["us_mean"] / 1e3, ratio=r["us_mean"] / full_us,
-                   ideal_ratio=step_bytes / bytes_full)
-        if forced_np is None:
-            ent["tau"] = tau
+        full_part = float(np.mean([(pt["forced_np"][t] * np.array(full_b)).sum() for t in range(K)]))
+    return local_b + gate_b + full_part, sum(full_all)
+
+
+def run_sweep(b, wl, args, full_us, gated_only=False, points=None):
+    """Time the step at every operating point: `reps` repetitions of the K
+    cold steps (the value is the median of the repetitions' means), then the
+    same K steps warm (back to back, no flush)."""
+    K = b.K
+    sweep = []
+    for pt in (points if points is not None else sweep_points(b, wl, args)):
+        calls = b.step_calls(pt["tau"], forced=pt["forced"], gated_only=gated_only)
+        reps = [b.timed(calls, args.warmup if i == 0 else 2, cold=True) for i in range(args.reps)]
+        means = [r["us_mean"] for r in reps]
+        per = np.concatenate([r["per_step"] for r in reps])
+        us = float(np.median(means))
+        recalled = reps[0]["recalled"]
+        real = recalled / (K * wl.batch)
+        nbytes, bytes_full = step_bytes(wl, b, pt, recalled, gated_only)
+        ent = dict(mode=pt["mode"], rho=pt["rho"], realised_rho=real, us=us, us_rep_min=min(means),
+                   us_rep_max=max(means), us_step_median=float(np.median(per)), us_step_min=float(per.min()),
+                   us_step_max=float(per.max()), GBps=nbytes / us / 1e3, ratio=us / full_us,
+                   ideal_ratio=nbytes / bytes_full)
+        if pt["mode"] == "tau":
+            ent["tau"] = pt["tau"]
         ent["hbm_frac"] = ent["GBps"] / HBM_PEAK_GBS
         ent["linearity"] = ent["ratio"] / ent["ideal_ratio"]
-        if args.warm:
-            w = b.timed(b.step_calls(tau, forced=forced), args.warmup, cold=False)
+        if not args.no_warm:
+            w = b.timed(calls, 2, cold=False)
             ent["warm_us"] = w["us_mean"]
             ent["warm_bracket_us"] = w["bracket_us"]
         sweep.append(ent)
-        log(f"[bench] {b.head} head rho={rho:.3f} (real {real:.3f}) {r['us_mean']:.1f} us/step ratio {ent['ratio']:.3f} "
-            f"ideal {ent['ideal_ratio']:.3f} x{ent['linearity']:.2f} {ent['GBps']:.0f} GB/s")
+        log(f"[bench] {b.head} head {pt['mode']} rho={pt['rho']:.3f} (real {real:.3f}) {us:.1f} us/step "
+            f"ratio {ent['ratio']:.3f} ideal {ent['ideal_ratio']:.3f} x{ent['linearity']:.2f} {ent['GBps']:.0f} GB/s"
+            + (" (retry on gated layers only)" if gated_only else ""))
     return sweep
+
+
+def run_per_layer(b, wl, args, points):
+    """The realism check: the same steps launched one layer per call, eager
+    and as a captured HIP graph."""
+    out = []
+    for pt in points:
+        eager, graph = b.per_layer(pt["tau"], pt["forced"], args.warmup)
+        ent = dict(mode=pt["mode"], rho=pt["rho"], realised_rho=eager["recalled"] / (b.K * wl.batch),
+                   eager_us=eager["us_mean"], graph_us=graph["us_mean"],
+                   graph_realised_rho=graph["recalled"] / (b.K * wl.batch))
+        out.append(ent)
+        log(f"[bench] per-layer launches rho={pt['rho']:.3f}: eager {eager['us_mean']:.1f} us/step, "
+            f"graph {graph['us_mean']:.1f} us/step")
+    return out
+
+
+def rounded(d, nd=4):
+    return {k: (round(v, nd) if isinstance(v, float) else v) for k, v in d.items()}
 
 
 PAPER_LENGTHS = (4139, 15918, 31400, 63852, 128852, 261696, 516788)
@@ -617,15 +882,17 @@ def decoder_bench(args):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--steps", type=int, default=0, help="timed steps per repetition (default: the workload's)")
     ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--reps", type=int, default=3, help="repetitions of the K steps per operating point")
     ap.add_argument("--config", default="llama3-8b")
     ap.add_argument("--head", default="paper", choices=["paper", "mlp"])
     ap.add_argument("--seed", type=int, default=1234)
     ap.add_argument("--split-blocks", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--warm", action="store_true", help="also time back-to-back (warm) steps")
+    ap.add_argument("--no-warm", action="store_true", help="skip the warm (back-to-back) timing of each point")
     ap.add_argument("--one-head", action="store_true", help="skip the second recall head's sweep")
+    ap.add_argument("--no-per-layer", action="store_true", help="skip the per-layer launch mode")
     ap.add_argument("--no-loop", action="store_true", help="skip the growing-context decode loop (graph) section")
     ap.add_argument("--loop-only", action="store_true", help="only the decode loop section (for profiling)")
     ap.add_argument("--decoder", action="store_true",
@@ -633,7 +900,8 @@ def main():
     ap.add_argument("--lengths", default="", help="--decoder: comma-separated context lengths")
     ap.add_argument("--decoder-steps", type=int, default=64, help="--decoder: timed steps per method")
     ap.add_argument("--roofline-only", action="store_true",
-                    help="only the roofline leg (always-Full calls) plus a 1 GiB copy, for PMC profiling")
+                    help="only the counter legs (Local, empty Full, the roofline Full launch) plus a 1 GiB copy, "
+                         "for PMC profiling")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
@@ -644,11 +912,21 @@ def main():
         decoder_bench(args)
         return
 
-    import torch
-
     from paper_2609_20734_amd import workloads as WL
     wl = WL.ALL[args.config]
-    K = args.steps
+    K = args.steps if args.steps > 0 else wl.steps
+    args.reps = max(1, args.reps)
+    pts_nominal = list(wl.bernoulli) if wl.bernoulli else list(wl.rhos)
+    head_rho = min(pts_nominal, key=lambda r: abs(r - HEADLINE_RHO)) if pts_nominal else 1.0
+
+    # the CPU oracle first: its process pool forks before the GPU is touched
+    cb = None
+    if not (args.no_cpu_baseline or args.roofline_only or args.loop_only):
+        cb = cpu_baseline(wl, args.head, args.seed, head_rho)
+        log(f"[bench] CPU oracle: {cb['value'] / 1e3:.1f} ms/step on 1 thread, {cb['pool']['value'] / 1e3:.1f} ms/step "
+            f"on {cb['pool']['cores']} processes (host: {cb['host_cpus']} CPUs, {cb['affinity_cpus']} usable)")
+
+    import torch
     b = Bench(wl, args.head, args.seed, K, args.split_blocks,
               growth=0 if (args.no_loop or args.roofline_only) else 16 * 8)
     P = b.P
@@ -656,6 +934,15 @@ def main():
     bytes_full = sum(full_b)
 
     if args.roofline_only:
+        # dispatch order (the counter summaries rely on it): 1 + R Local launches,
+        # 1 + R empty Full launches (list of zero requests), 1 + R roofline
+        # launches (Full over every request), then three 1 GiB copies
+        t_loc = b.kernel_time([P.prepare_local(s.shape, s.inp, *s.local_args, s.out, s.lse, s.ws_local)
+                               for s in b.stacks], reps=ROOFLINE_REPS, cold=True)
+        b.n_work.zero_()
+        t_empty = b.kernel_time([P.prepare_full(s.shape, s.inp, s.stack.native_window, None, b.work, b.n_work,
+                                                s.out, s.lse, s.ws_full) for s in b.stacks],
+                                reps=ROOFLINE_REPS, cold=True)
         t = b.kernel_time(b.full_calls()[0], reps=ROOFLINE_REPS, cold=True)
         src = torch.ones(1 << 28, dtype=torch.float32, device=b.dev)
         dst = torch.empty_like(src)
@@ -663,7 +950,8 @@ def main():
             dst.copy_(src)          # calibration: 1 GiB read + 1 GiB written
         torch.cuda.synchronize()
         print(json.dumps({"roofline_only": True, "kernel": ROOFLINE_KERNEL, "us_per_launch": t,
-                          "bytes_per_launch": bytes_full, "reps": ROOFLINE_REPS,
+                          "bytes_per_launch": bytes_full, "reps": ROOFLINE_REPS, "local_us": t_loc,
+                          "local_bytes": local_b, "empty_full_us": t_empty,
                           "copy_bytes": 1 << 30, "source_sha256": source_sha256()}), flush=True)
         return
 
@@ -672,62 +960,86 @@ def main():
         return
 
     # always-Full baseline
-    full = b.timed(b.full_calls(), args.warmup, cold=True)
-    log(f"[bench] always-Full {full['us_mean']:.1f} us/step ({bytes_full / full['us_mean'] / 1e3:.0f} GB/s)")
+    fulls = [b.timed(b.full_calls(), args.warmup if i == 0 else 2, cold=True) for i in range(args.reps)]
+    full_us = float(np.median([f["us_mean"] for f in fulls]))
+    log(f"[bench] always-Full {full_us:.1f} us/step ({bytes_full / full_us / 1e3:.0f} GB/s)")
 
-    # rho sweep with the App. A.2 head (headline), then the MLP stand-in
+    # operating points with the App. A.2 head (headline), then the MLP stand-in
     head0 = args.head
-    sweep = run_sweep(b, wl, args, full["us_mean"])
+    pts = sweep_points(b, wl, args)
+    sweep = run_sweep(b, wl, args, full_us, points=pts)
+    primary = [p for p in pts if p["mode"] == primary_mode(wl)]
+    gated_only = []
+    if any(not st.gated for st in wl.stacks):
+        gated_only = run_sweep(b, wl, args, full_us, gated_only=True, points=primary)
+    per_layer = [] if args.no_per_layer else run_per_layer(b, wl, args, primary)
     other = "mlp" if head0 == "paper" else "paper"
     sweep_other = []
     if not args.one_head:
         b.set_head(other)
-        sweep_other = run_sweep(b, wl, args, full["us_mean"])
+        sweep_other = run_sweep(b, wl, args, full_us)
         b.set_head(head0)
 
     loop = [] if args.no_loop else b.decode_loop()
     layout = b.local_layout()
     log(f"[bench] Local alone, cold: permuted block table {layout['permuted_us']:.1f} us, "
         f"contiguous table {layout['contiguous_us']:.1f} us")
+    sinks = b.local_sinks()
+    log(f"[bench] Local alone, cold: s={sinks['n_sink']} {sinks['sinks_us']:.1f} us, s=0 {sinks['no_sinks_us']:.1f} us")
 
     # roofline of the dominant kernel: the Full split-K pass over every request
     # (one launch of attn_split_kernel<128, false>; no merge launch at this size),
     # the last ROOFLINE_REPS dispatches of that kernel in this process
     fcalls = b.full_calls()[0]
     t_full_call = b.kernel_time(fcalls, reps=ROOFLINE_REPS, cold=True)
+    ceil_full = b.read_ceiling(bytes_full)
+    ceil_local = b.read_ceiling(local_b)
+    log(f"[bench] streaming-read ceiling: {ceil_full['GBps']:.0f} GB/s over {ceil_full['bytes'] / 1e9:.2f} GB, "
+        f"{ceil_local['GBps']:.0f} GB/s over {ceil_local['bytes'] / 1e6:.0f} MB")
     roof = dict(bound="hbm", achieved=bytes_full / t_full_call / 1e3, peak=HBM_PEAK_GBS, unit="GB/s",
                 traffic=measured_traffic())
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["kernel"] = ROOFLINE_KERNEL + " (oda_full_decode_attn, every request)"
     roof["bytes_per_launch"] = bytes_full
     roof["us_per_launch"] = t_full_call
+    roof["read_ceiling_GBps"] = ceil_full["GBps"]
+    roof["frac_of_read_ceiling"] = roof["achieved"] / ceil_full["GBps"]
 
-    head_ent = min(sweep, key=lambda e: abs(e["rho"] - HEADLINE_RHO)) if sweep else None
-    value = head_ent["us"] if head_ent else full["us_mean"]
+    prim = [e for e in sweep if e["mode"] == primary_mode(wl)]
+    head_ent = min(prim, key=lambda e: abs(e["rho"] - HEADLINE_RHO)) if prim else None
+    value = head_ent["us"] if head_ent else full_us
+    nset = sorted(set(b.seq_host.tolist()))
     res = {
         "metric": METRIC, "value": round(value, 3), "unit": "us/step", "n_gpus": 1, "steps": K,
-        "warmup": args.warmup, "ms_per_step": round(value / 1e3, 6), "higher_is_better": False, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "warmup": args.warmup, "reps": args.reps, "ms_per_step": round(value / 1e3, 6), "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{wl.name}: {wl.num_layers} layers, B={wl.batch}, {wl.num_q_heads}q/{wl.num_kv_heads}kv "
-                               f"heads, D={wl.head_dim}, n={'/'.join(str(x) for x in sorted(set(b.seq_host.tolist()))[:4])}"
-                               f"{'...' if len(set(b.seq_host.tolist())) > 4 else ''}, "
+                               f"heads, D={wl.head_dim}, n={'/'.join(str(x) for x in nset[:4])}"
+                               f"{'...' if len(nset) > 4 else ''}, "
                                f"W={wl.stacks[-1].local_window}, s={wl.stacks[-1].local_sink}, paged bf16 KV "
                                f"(block 16, permuted), {args.head} recall head {wl.d_model}->{wl.d_hidden}->1, "
-                               f"rho={head_ent['rho'] if head_ent else 1.0}, cold (Infinity Cache flushed between steps)",
+                               f"{head_ent['mode'] + ' ' if head_ent else ''}rho={head_ent['rho'] if head_ent else 1.0}, "
+                               f"cold (Infinity Cache flushed between steps)",
                    "head": args.head, "seed": args.seed, "split_blocks": args.split_blocks},
         "GBps": round(head_ent["GBps"], 1) if head_ent else None,
-        "always_full_us": round(full["us_mean"], 3),
-        "always_full_GBps": round(bytes_full / full["us_mean"] / 1e3, 1),
-        "sweep": [{k: (round(v, 4) if isinstance(v, float) else v) for k, v in e.items()} for e in sweep],
-        f"sweep_{other}_head": [{k: (round(v, 4) if isinstance(v, float) else v) for k, v in e.items()}
-                                for e in sweep_other],
-        "decode_loop": [{k: (round(v, 3) if isinstance(v, float) else v) for k, v in e.items()} for e in loop],
-        "local_window_layout": {k: round(v, 3) for k, v in layout.items()},
-        "roofline": {k: (round(v, 4) if isinstance(v, float) else v) for k, v in roof.items()},
+        "always_full_us": round(full_us, 3),
+        "always_full_us_reps": [round(f["us_mean"], 3) for f in fulls],
+        "always_full_GBps": round(bytes_full / full_us / 1e3, 1),
+        "sweep": [rounded(e) for e in sweep],
+        f"sweep_{other}_head": [rounded(e) for e in sweep_other],
+        "per_layer": [rounded(e, 3) for e in per_layer],
+        "decode_loop": [rounded(e, 3) for e in loop],
+        "local_window_layout": rounded(layout, 3),
+        "local_sinks": rounded(sinks, 3),
+        "read_ceiling": {"full_size": rounded(ceil_full, 3), "local_size": rounded(ceil_local, 3)},
+        "roofline": rounded(roof),
     }
-    if not args.no_cpu_baseline:
-        cb = cpu_baseline(b, head_ent["rho"] if head_ent else 1.0)
-        res["cpu_baseline"] = {k: (round(v, 3) if isinstance(v, float) else v) for k, v in cb.items()}
+    if gated_only:
+        res["sweep_gated_only"] = [rounded(e) for e in gated_only]
+    if cb is not None:
+        cbr = rounded(cb, 3)
+        cbr["pool"] = rounded(cb["pool"], 3)
+        res["cpu_baseline"] = cbr
     print(json.dumps(res), flush=True)
 
 

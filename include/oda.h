@@ -287,6 +287,18 @@ oda_status oda_copy_rows(int32_t batch, int32_t row_len, const float *src, float
  * (-1 if all are NaN); x fp32 [batch][n], n a multiple of 4. */
 oda_status oda_argmax(int32_t batch, int32_t n, const float *x, int32_t *index, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Measurement aid (not a step of the method): the streaming-read ceiling that
+ * the attention kernels' bandwidth is quoted against.
+ * ------------------------------------------------------------------------- */
+
+/* Reads `bytes` of device memory at src once (16-byte nontemporal loads, the
+ * attention kernels' KV loads) and discards them.  src 16-byte aligned, bytes a
+ * multiple of 16; sink: device uint32[1], left unchanged in practice (written
+ * only if the XOR of everything read hits one fixed value); groups: workgroups
+ * of 256 threads, 0 for the default (256). */
+oda_status oda_stream_read(const void *src, size_t bytes, uint32_t *sink, int32_t groups, hipStream_t stream);
+
 /* Static description of a status code. */
 const char *oda_status_string(oda_status status);
 

@@ -36,7 +36,7 @@ DENSE_SWIGLU = 1
 EXPORTED = ("oda_attn_workspace_size", "oda_local_decode_attn", "oda_full_decode_attn",
             "oda_gate_param_count", "oda_gate_workspace_size", "oda_recall_gate", "oda_commit_kv",
             "oda_dense_bf16", "oda_qk_norm_rope", "oda_embed_bf16", "oda_copy_rows", "oda_argmax",
-            "oda_status_string", "oda_last_error")
+            "oda_stream_read", "oda_status_string", "oda_last_error")
 
 
 class OdaError(RuntimeError):
@@ -107,6 +107,8 @@ _lib.oda_copy_rows.argtypes = [ctypes.c_int32, ctypes.c_int32, _V, _V, _V, _V, _
 _lib.oda_copy_rows.restype = ctypes.c_int
 _lib.oda_argmax.argtypes = [ctypes.c_int32, ctypes.c_int32, _V, _V, _V]
 _lib.oda_argmax.restype = ctypes.c_int
+_lib.oda_stream_read.argtypes = [_V, ctypes.c_size_t, _V, ctypes.c_int32, _V]
+_lib.oda_stream_read.restype = ctypes.c_int
 _lib.oda_status_string.argtypes = [ctypes.c_int]
 _lib.oda_status_string.restype = ctypes.c_char_p
 _lib.oda_last_error.argtypes = []
@@ -271,6 +273,11 @@ def argmax(batch: int, n: int, x, index, stream=None) -> None:
     _check(_lib.oda_argmax(batch, n, _ptr(x), _ptr(index), _stream(stream)))
 
 
+def stream_read(src, nbytes: int, sink, groups: int = 0, stream=None) -> None:
+    """Measurement aid: read nbytes of src once (the streaming-read ceiling)."""
+    _check(_lib.oda_stream_read(_ptr(src), int(nbytes), _ptr(sink), groups, _stream(stream)))
+
+
 # ---------------------------------------------------------------------------
 # pre-marshalled calls (for tight launch loops: no per-call conversion)
 # ---------------------------------------------------------------------------
@@ -357,3 +364,8 @@ def prepare_copy_rows(batch: int, row_len: int, src, dst, work_list=None, n_work
 def prepare_argmax(batch: int, n: int, x, index, stream=None) -> Call:
     args = (batch, n, _ptr(x), _ptr(index), _stream(stream))
     return Call(_lib.oda_argmax, args, (x, index))
+
+
+def prepare_stream_read(src, nbytes: int, sink, groups: int = 0, stream=None) -> Call:
+    args = (_ptr(src), int(nbytes), _ptr(sink), groups, _stream(stream))
+    return Call(_lib.oda_stream_read, args, (src, sink))

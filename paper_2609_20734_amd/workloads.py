@@ -32,7 +32,8 @@ class Workload:
     d_model: int = 0
     d_hidden: int = 0
     rhos: tuple = ()                  # recall rates swept via the threshold
-    bernoulli: tuple = ()             # per-request forced-flag probabilities
+    bernoulli: tuple = ()             # per-request forced-flag probabilities (when set, the headline
+                                      # operating points; threshold-driven rates are reported beside them)
     steps: int = 16
     extra: dict = field(default_factory=dict)
 
@@ -52,7 +53,8 @@ LLAMA = Workload("llama3-8b", batch=1, num_q_heads=32, num_kv_heads=8, head_dim=
                  seq_lens=(32768,), d_model=4096, d_hidden=256, rhos=(0.0, 0.1, 0.25, 0.5, 1.0), steps=1000)
 
 MIXED = Workload("mixed", batch=32, num_q_heads=32, num_kv_heads=8, head_dim=128, stacks=(_gated(32, 2048),),
-                 seq_range=(8192, 65536), d_model=4096, d_hidden=256, bernoulli=(0.1, 0.25, 0.5), steps=50)
+                 seq_range=(8192, 65536), d_model=4096, d_hidden=256, rhos=(0.1, 0.25, 0.5),
+                 bernoulli=(0.1, 0.25, 0.5), steps=50)
 
 LONG = Workload("long", batch=4, num_q_heads=32, num_kv_heads=8, head_dim=128, stacks=(_gated(32, 4096),),
                 seq_lens=(131072,) * 4, d_model=4096, d_hidden=256, rhos=(0.0, 0.05, 0.2, 1.0), steps=100)

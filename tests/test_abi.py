@@ -197,3 +197,17 @@ def test_decoder_entry_points_reject_bad_arguments(L):
     assert status_of(lambda: L.copy_rows(2, 8, x, y, 0x40000, None, stream=0)) == -1
     assert status_of(lambda: L.argmax(2, 10, x, y, stream=0)) == -2
     assert status_of(lambda: L.argmax(0, 8, x, y, stream=0)) == -2
+
+
+def test_stream_read_rejects_bad_arguments(L):
+    def status_of_read(src=0x10000, nbytes=4096, sink=0x20000, groups=0):
+        with pytest.raises(L.OdaError) as e:
+            L.stream_read(src, nbytes, sink, groups, stream=0)
+        return e.value.status
+
+    assert status_of_read(src=None) == -1
+    assert status_of_read(sink=None) == -1
+    assert status_of_read(src=0x10008) == -2                  # misaligned
+    assert status_of_read(nbytes=4100) == -2                  # not a multiple of 16
+    assert status_of_read(groups=-1) == -2
+    L.stream_read(0x10000, 0, 0x20000, 0, stream=0)           # nothing to read: no launch

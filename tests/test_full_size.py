@@ -134,3 +134,48 @@ def test_hybrid_full_size():
     off = int(np.flatnonzero(~flags)[0])
     # stack 0: native sliding-window layers; stack 1: global, ODA-gated layers
     _check_rows(b, flags, [(0, 0, off), (0, 35, on), (1, 0, on), (1, 11, off)])
+
+
+def test_llama_per_layer_launches_eager_and_graph():
+    """The per-layer launch mode (one call per layer, the gate reading staged
+    inputs): parity with the oracle, and a captured graph of it replays to the
+    eager result bit for bit."""
+    b = _bench("llama3-8b")
+    st = b.stacks[0]
+    b.h_stage.copy_(b.h[0])
+    b.e_stage.copy_(b.e[0])
+    b.l_stage.copy_(b.l[0])
+    for tau in (math.inf, -math.inf):
+        for c in b.per_layer_calls(tau, None):
+            c()
+        torch.cuda.synchronize()
+        flags = _check_gate(b, tau)
+        _check_rows(b, flags, [(0, 0, 0), (0, 19, 0), (0, 31, 0)])
+    eager = st.out.clone(), st.lse.clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for c in b.per_layer_calls(-math.inf, None):
+            c()
+    for _ in range(3):
+        st.out.fill_(0.0)
+        st.lse.fill_(0.0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(st.out, eager[0]) and torch.equal(st.lse, eager[1])
+    del g
+
+
+def test_hybrid_retry_on_gated_layers_only():
+    """The gated-only retry variant: the natively windowed layers keep their
+    (already native) Local result, the gated layers of flagged requests get
+    Full."""
+    b = _bench("hybrid")
+    tau = _median_tau(b)
+    for c in b.step_calls(tau, gated_only=True)[0]:
+        c()
+    torch.cuda.synchronize()
+    flags = _check_gate(b, tau)
+    on = int(np.flatnonzero(flags)[0])
+    off = int(np.flatnonzero(~flags)[0])
+    _check_rows(b, flags, [(0, 3, on), (0, 20, off), (1, 2, on), (1, 7, off)])
