@@ -110,8 +110,8 @@ class StackState:
         loc_w = stack.native_window if not stack.gated else stack.local_window
         loc_s = 0 if not stack.gated else stack.local_sink
         self.local_args = (loc_s, loc_w)
-        self.ws_local = torch.empty(P.attn_workspace_size(self.shape, loc_s, loc_w), dtype=torch.uint8, device=dev)
-        self.ws_full = torch.empty(P.attn_workspace_size(self.shape, 0, stack.native_window), dtype=torch.uint8,
+        self.ws_local = torch.zeros(P.attn_workspace_size(self.shape, loc_s, loc_w), dtype=torch.uint8, device=dev)
+        self.ws_full = torch.zeros(P.attn_workspace_size(self.shape, 0, stack.native_window), dtype=torch.uint8,
                                    device=dev)
 
 
@@ -356,9 +356,9 @@ class Bench:
                 s = st.shape
                 sh = P.Shape(1, s.batch, s.num_q_heads, s.num_kv_heads, s.head_dim, s.max_blocks_per_seq,
                              s.max_seq_len, s.num_blocks, s.split_blocks)
-                ws_l = torch.empty(max(256, P.attn_workspace_size(sh, *st.local_args)), dtype=torch.uint8,
+                ws_l = torch.zeros(max(256, P.attn_workspace_size(sh, *st.local_args)), dtype=torch.uint8,
                                    device=self.dev)
-                ws_f = torch.empty(max(256, P.attn_workspace_size(sh, 0, st.stack.native_window)),
+                ws_f = torch.zeros(max(256, P.attn_workspace_size(sh, 0, st.stack.native_window)),
                                    dtype=torch.uint8, device=self.dev)
                 ins = [P.inputs(st.q[l], st.k[l], st.v[l], self.dtable, self.dseq, scale)
                        for l in range(st.stack.num_layers)]
@@ -406,6 +406,28 @@ class Bench:
         del g
         return eager, graph
 
+    def per_layer_full(self, warmup):
+        """Always-Full in the per-layer launch mode: one Full call per layer over
+        every request, no Local, no gate; eager and as a captured graph."""
+        torch, P = self.torch, self.P
+
+        def calls():
+            out = []
+            for st, sh, _, ws_f, ins in self._layer_state():
+                out += [P.prepare_full(sh, inp, st.stack.native_window, None, None, None, st.out[l], st.lse[l],
+                                       ws_f) for l, inp in enumerate(ins)]
+            return out
+
+        eager = self.timed([calls()] * self.K, warmup, cold=True)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for c in calls():
+                c()
+        graph = self.timed([[g.replay]] * self.K, warmup, cold=True)
+        del g
+        return eager, graph
+
     # -- single measurements -------------------------------------------------------
     def local_sinks(self, reps=20):
         """Local alone (every layer group, cold) with the configured sinks and
@@ -418,7 +440,7 @@ class Bench:
                 s_, w_ = st.local_args
                 if zero:
                     s_ = 0
-                ws = torch.empty(max(256, P.attn_workspace_size(st.shape, s_, w_)), dtype=torch.uint8,
+                ws = torch.zeros(max(256, P.attn_workspace_size(st.shape, s_, w_)), dtype=torch.uint8,
                                  device=self.dev)
                 calls.append(P.prepare_local(st.shape, st.inp, s_, w_, st.out, st.lse, ws))
             res[f"{name}_us"] = self.kernel_time(calls, reps, cold=True)
@@ -714,17 +736,21 @@ def run_sweep(b, wl, args, full_us, gated_only=False, points=None):
 
 def run_per_layer(b, wl, args, points):
     """The realism check: the same steps launched one layer per call, eager
-    and as a captured HIP graph."""
+    and as a captured HIP graph, against always-Full launched the same way."""
+    fe, fg = b.per_layer_full(args.warmup)
+    base = dict(eager_us=fe["us_mean"], graph_us=fg["us_mean"])
+    log(f"[bench] per-layer always-Full: eager {fe['us_mean']:.1f} us/step, graph {fg['us_mean']:.1f} us/step")
     out = []
     for pt in points:
         eager, graph = b.per_layer(pt["tau"], pt["forced"], args.warmup)
         ent = dict(mode=pt["mode"], rho=pt["rho"], realised_rho=eager["recalled"] / (b.K * wl.batch),
                    eager_us=eager["us_mean"], graph_us=graph["us_mean"],
-                   graph_realised_rho=graph["recalled"] / (b.K * wl.batch))
+                   graph_realised_rho=graph["recalled"] / (b.K * wl.batch),
+                   eager_ratio=eager["us_mean"] / fe["us_mean"], graph_ratio=graph["us_mean"] / fg["us_mean"])
         out.append(ent)
         log(f"[bench] per-layer launches rho={pt['rho']:.3f}: eager {eager['us_mean']:.1f} us/step, "
-            f"graph {graph['us_mean']:.1f} us/step")
-    return out
+            f"graph {graph['us_mean']:.1f} us/step (x{ent['eager_ratio']:.3f} of per-layer always-Full)")
+    return base, out
 
 
 def rounded(d, nd=4):
@@ -972,7 +998,7 @@ def main():
     gated_only = []
     if any(not st.gated for st in wl.stacks):
         gated_only = run_sweep(b, wl, args, full_us, gated_only=True, points=primary)
-    per_layer = [] if args.no_per_layer else run_per_layer(b, wl, args, primary)
+    per_layer_full, per_layer = (None, []) if args.no_per_layer else run_per_layer(b, wl, args, primary)
     other = "mlp" if head0 == "paper" else "paper"
     sweep_other = []
     if not args.one_head:
@@ -1028,6 +1054,7 @@ def main():
         "sweep": [rounded(e) for e in sweep],
         f"sweep_{other}_head": [rounded(e) for e in sweep_other],
         "per_layer": [rounded(e, 3) for e in per_layer],
+        "per_layer_always_full": rounded(per_layer_full, 3) if per_layer_full else None,
         "decode_loop": [rounded(e, 3) for e in loop],
         "local_window_layout": rounded(layout, 3),
         "local_sinks": rounded(sinks, 3),

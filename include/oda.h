@@ -33,9 +33,11 @@
  *     attention writes NaN rows (out and lse) for a request whose length or
  *     used table entry is out of range, the commit writes nothing for it, and
  *     listed requests outside the batch are skipped.
- *   - The library keeps no state between calls.  Workspaces may be reused by
- *     later calls on the same stream; calls that share a workspace must not
- *     overlap in time.
+ *   - The library keeps no state between calls other than what a caller's
+ *     workspace holds: attention workspaces carry merge-ticket words that
+ *     every call leaves zero (see oda_attn_workspace_size).  Workspaces may be
+ *     reused by later calls on the same stream; calls that share a workspace
+ *     must not overlap in time.
  *   - Results are deterministic: a fixed split order, no floating-point
  *     atomics; reruns are bit-identical.
  *
@@ -108,10 +110,17 @@ typedef struct {
 } oda_attn_inputs;
 
 /* Bytes of workspace an attention call with this shape and access set needs
- * (split-K partials).  It is 0 when every request fits one work item; the
- * workspace pointer may then be NULL.  window == 0 means "no window" (the whole
+ * (one merge-ticket word per (layer, request, KV head), then the split-K
+ * partials).  It is 0 when every request fits one work item; the workspace
+ * pointer may then be NULL.  window == 0 means "no window" (the whole
  * history); window > 0 limits the recent part to `window` positions.
- * n_sink >= 0.  (host out) */
+ * n_sink >= 0.  (host out)
+ * A workspace must be zero-filled before its first use (e.g. allocated
+ * zeroed).  Every call leaves its ticket words zero again, so later calls on
+ * the same stream with the same num_layers * batch * num_kv_heads (any sinks,
+ * window or branch) reuse it as it is, graph replays included; zero it again
+ * before using it with a larger product.  Calls that may run concurrently
+ * need separate workspaces. */
 oda_status oda_attn_workspace_size(const oda_attn_shape *shape, int32_t n_sink, int32_t window,
                                    size_t *bytes);
 

@@ -11,10 +11,10 @@
 //             The wavefronts then combine their (m, l, o) through LDS.  If the
 //             item covers the request's whole access set the workgroup writes
 //             out / lse directly (adding the uncommitted current candidate);
-//             otherwise it writes an unnormalised partial.
-//   merge  -- only when some request needs several splits: one workgroup per
-//             (layer, request, KV head) combines the partials with stable
-//             softmax rescaling (plus the candidate) and writes out / lse.
+//             otherwise it writes an unnormalised partial, takes a ticket,
+//             and the workgroup holding the request's last ticket combines
+//             the partials in split order with stable softmax rescaling (plus
+//             the candidate) and writes out / lse: no second launch.
 // This is the split-phase / combine-phase structure the paper's Local path
 // uses (App. A.5), applied to both branches.
 //
@@ -42,6 +42,9 @@
 #endif
 #ifndef ODA_SPLIT_PREFETCH
 #define ODA_SPLIT_PREFETCH 0
+#endif
+#ifndef ODA_FUSED_MERGE
+#define ODA_FUSED_MERGE 1   // 0: merge split-K partials in a second launch
 #endif
 #ifndef ODA_SPLIT_WAVES
 #define ODA_SPLIT_WAVES 8
@@ -81,6 +84,7 @@ struct AttnArgs {
   float* lse;
   float* part_o;     // [L][B][Hkv][max_splits][G][D]
   float* part_ml;    // [L][B][Hkv][max_splits][G][2]  (m in log2 units, l)
+  uint32_t* tickets; // [L][B][Hkv] splits finished so far (zero between calls)
   int64_t kv_layer_stride;  // elements between layers of k_cache / v_cache
   int32_t L, B, Hq, Hkv, G, MB;
   int32_t n_sink, window;   // window <= 0: no window
@@ -369,6 +373,60 @@ __host__ __device__ constexpr size_t split_lds_floats(int G, int D) {
   return (size_t)kWaves * 32 + (size_t)kWaves * G * D + 16;
 }
 
+// Combine the nsplit partials of one (layer, request, KV head) with stable
+// softmax rescaling (plus the uncommitted candidate) and write out / lse.
+// Called by every thread of a workgroup of `nthreads` threads (it holds a
+// barrier); sm_zc: LDS for kMaxGroup candidate logits.  Partials are read in
+// split order, so the result does not depend on which workgroup merges.
+template <int D>
+__device__ __forceinline__ void merge_unit(const AttnArgs& a, int l, int b, int g, int nsplit, float* sm_zc,
+                                           int nthreads) {
+  const int G = a.G;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t pbase = (((int64_t)l * a.B + b) * a.Hkv + g) * a.max_splits;
+  const float* ml = a.part_ml + pbase * G * 2;
+  const float* po = a.part_o + pbase * G * D;
+  const int64_t qoff = (((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G) * D;
+  const int64_t coff = (((int64_t)l * a.B + b) * a.Hkv + g) * D;
+
+  if (a.has_cur) {
+    constexpr int PD = D / 64;
+    float kc[PD];
+#pragma unroll
+    for (int e = 0; e < PD; ++e) kc[e] = bf16_to_float(a.k_cur[coff + lane * PD + e]);
+    for (int hh = wave; hh < G; hh += nthreads / 64) {
+      float dot = 0.f;
+#pragma unroll
+      for (int e = 0; e < PD; ++e) dot += bf16_to_float(a.q[qoff + hh * D + lane * PD + e]) * kc[e];
+      dot = wave_sum(dot) * a.scale_log2;
+      if (lane == 0) sm_zc[hh] = dot;
+    }
+  }
+  __syncthreads();
+
+  for (int e = threadIdx.x; e < G * D; e += nthreads) {
+    const int hh = e / D, d = e - hh * D;
+    float M = a.has_cur ? sm_zc[hh] : -INFINITY;
+    for (int s = 0; s < nsplit; ++s) M = fmaxf(M, ml[(s * G + hh) * 2]);
+    float acc = 0.f, lam = 0.f;
+#pragma unroll 4
+    for (int s = 0; s < nsplit; ++s) {
+      const float w = exp2_fast(ml[(s * G + hh) * 2] - M);
+      acc += w * po[((int64_t)s * G + hh) * D + d];
+      lam += w * ml[(s * G + hh) * 2 + 1];
+    }
+    if (a.has_cur) {
+      const float w = exp2_fast(sm_zc[hh] - M);
+      acc += w * bf16_to_float(a.v_cur[coff + d]);
+      lam += w;
+    }
+    a.out[qoff + e] = acc / lam;
+    if (d == 0 && a.lse != nullptr)
+      a.lse[((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G + hh] = (M + __log2f(lam)) * kLn2;
+  }
+}
+
 // kLocal selects the Local access set (sinks + window); Full instances take the
 // native set (whole history, or a native window) and never have sinks.
 template <int D, bool kLocal>
@@ -560,10 +618,35 @@ void attn_split_kernel(AttnArgs a) {
       }
     }
   }
+#if ODA_FUSED_MERGE
+  if (finalize) return;
+  // The last of the request's splits to finish merges them all.  The eight
+  // XCDs' L2 caches are not coherent with each other, so the partials are
+  // published at device scope: every wavefront waits until its stores have
+  // reached its XCD's L2, then one thread writes that L2 back (one release per
+  // workgroup: a release per wavefront made one-layer Full calls over 32K
+  // positions ~40% slower) and takes a ticket.  The workgroup holding the last ticket
+  // drops stale cached lines (acquire), merges, and sets the count back to 0.
+  __shared__ int last_split;
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  uint32_t* ticket = a.tickets + ((int64_t)l * a.B + b) * a.Hkv + g;
+  if (threadIdx.x == 0) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    const uint32_t t = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    last_split = (t == (uint32_t)(nsplit - 1)) ? 1 : 0;
+  }
+  __syncthreads();
+  if (!last_split) return;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  merge_unit<D>(a, l, b, g, nsplit, sm_zc, kWaves * 64);
+  if (threadIdx.x == 0) __hip_atomic_store(ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#endif
 }
 
+#if !ODA_FUSED_MERGE
 // One workgroup per (layer, request slot, KV head) whose request has several
-// splits: thread e owns entries e, e + 256, ... of the [G][D] block.
+// splits.
 template <int D>
 __global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(AttnArgs a) {
   __shared__ float sm_zc[kMaxGroup];
@@ -582,51 +665,9 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(AttnArgs a) {
   const int bps = effective_bps(a);
   const int nsplit = max(1, (geo.nvb + bps - 1) / bps);
   if (nsplit <= 1) return;   // finalized by the split kernel
-  const int G = a.G;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int64_t pbase = (((int64_t)l * a.B + b) * a.Hkv + g) * a.max_splits;
-  const float* ml = a.part_ml + pbase * G * 2;
-  const float* po = a.part_o + pbase * G * D;
-  const int64_t qoff = (((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G) * D;
-  const int64_t coff = (((int64_t)l * a.B + b) * a.Hkv + g) * D;
-
-  if (a.has_cur) {
-    constexpr int PD = D / 64;
-    float kc[PD];
-#pragma unroll
-    for (int e = 0; e < PD; ++e) kc[e] = bf16_to_float(a.k_cur[coff + lane * PD + e]);
-    for (int hh = wave; hh < G; hh += kMergeThreads / 64) {
-      float dot = 0.f;
-#pragma unroll
-      for (int e = 0; e < PD; ++e) dot += bf16_to_float(a.q[qoff + hh * D + lane * PD + e]) * kc[e];
-      dot = wave_sum(dot) * a.scale_log2;
-      if (lane == 0) sm_zc[hh] = dot;
-    }
-    __syncthreads();
-  }
-
-  for (int e = threadIdx.x; e < G * D; e += kMergeThreads) {
-    const int hh = e / D, d = e - hh * D;
-    float M = a.has_cur ? sm_zc[hh] : -INFINITY;
-    for (int s = 0; s < nsplit; ++s) M = fmaxf(M, ml[(s * G + hh) * 2]);
-    float acc = 0.f, lam = 0.f;
-#pragma unroll 4
-    for (int s = 0; s < nsplit; ++s) {
-      const float w = exp2_fast(ml[(s * G + hh) * 2] - M);
-      acc += w * __builtin_nontemporal_load(po + ((int64_t)s * G + hh) * D + d);
-      lam += w * ml[(s * G + hh) * 2 + 1];
-    }
-    if (a.has_cur) {
-      const float w = exp2_fast(sm_zc[hh] - M);
-      acc += w * bf16_to_float(a.v_cur[coff + d]);
-      lam += w;
-    }
-    a.out[qoff + e] = acc / lam;
-    if (d == 0 && a.lse != nullptr)
-      a.lse[((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G + hh] = (M + __log2f(lam)) * kLn2;
-  }
+  merge_unit<D>(a, l, b, g, nsplit, sm_zc, kMergeThreads);
 }
+#endif
 
 // ---------------------------------------------------------------------------
 // host side
@@ -637,6 +678,7 @@ struct Plan {
   int bps;
   int max_splits;
   int dyn;
+  size_t off_o;
   size_t off_ml;
   size_t bytes;
 };
@@ -693,6 +735,7 @@ void make_plan(const oda_attn_shape* s, int n_sink, int window, Plan* p) {
   p->bps = (int)std::min<int64_t>(bps, 1 << 30);
   p->max_splits = (int)oda::ceil_div(nvb, bps);
   if (p->max_splits <= 1) {
+    p->off_o = 0;
     p->off_ml = 0;
     p->bytes = 0;
     return;
@@ -701,8 +744,12 @@ void make_plan(const oda_attn_shape* s, int n_sink, int window, Plan* p) {
   const int64_t parts = units * p->max_splits * G;
   const int64_t o_bytes = oda::round_up(parts * s->head_dim * 4, 256);
   const int64_t ml_bytes = oda::round_up(parts * 2 * 4, 256);
-  p->off_ml = (size_t)o_bytes;
-  p->bytes = (size_t)(o_bytes + ml_bytes);
+  // ticket words first: their place depends only on L * B * Hkv, so a
+  // workspace stays valid across calls that differ in sinks or window
+  const int64_t t_bytes = ODA_FUSED_MERGE ? oda::round_up(units * 4, 256) : 0;
+  p->off_o = (size_t)t_bytes;
+  p->off_ml = (size_t)(t_bytes + o_bytes);
+  p->bytes = (size_t)(t_bytes + o_bytes + ml_bytes);
 }
 
 oda_status check_inputs(const oda_attn_inputs* in, const float* out) {
@@ -733,8 +780,10 @@ oda_status launch(const AttnArgs& args, const Plan& plan, hipStream_t stream) {
   }
   (void)hipGetLastError();
   hipLaunchKernelGGL((attn_split_kernel<D, kLocal>), dim3((unsigned)items), dim3(kWaves * 64), lds, stream, args);
+#if !ODA_FUSED_MERGE
   if (plan.max_splits > 1)
     hipLaunchKernelGGL(attn_merge_kernel<D>, dim3((unsigned)units), dim3(kMergeThreads), 0, stream, args);
+#endif
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return oda::fail(ODA_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ODA_OK;
@@ -764,8 +813,9 @@ oda_status run_attention(const oda_attn_shape* s, const oda_attn_inputs* in, boo
   a.n_work = n_work;
   a.out = out;
   a.lse = lse;
-  a.part_o = static_cast<float*>(ws);
+  a.part_o = plan.bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + plan.off_o) : nullptr;
   a.part_ml = plan.bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + plan.off_ml) : nullptr;
+  a.tickets = (plan.bytes != 0 && ODA_FUSED_MERGE != 0) ? static_cast<uint32_t*>(ws) : nullptr;
   a.kv_layer_stride = s->num_blocks * s->num_kv_heads * kBlock * s->head_dim;
   a.max_len = s->max_seq_len;
   a.num_blocks = s->num_blocks;

@@ -104,9 +104,9 @@ class Decoder:
                                                              device=dev)
         # one-layer attention calls: the layer's slices of the caches and candidates
         self.attn_shape = P.Shape(1, B, Hq, Hkv, D, max_blocks_per_seq, max_seq_len, num_blocks, split_blocks)
-        self.ws_local = torch.empty(max(256, P.attn_workspace_size(self.attn_shape, n_sink, window)),
+        self.ws_local = torch.zeros(max(256, P.attn_workspace_size(self.attn_shape, n_sink, window)),
                                     dtype=torch.uint8, device=dev)
-        self.ws_full = torch.empty(max(256, P.attn_workspace_size(self.attn_shape, 0, 0)), dtype=torch.uint8,
+        self.ws_full = torch.zeros(max(256, P.attn_workspace_size(self.attn_shape, 0, 0)), dtype=torch.uint8,
                                    device=dev)
         self.scale = 1.0 / math.sqrt(D)
         w = weights

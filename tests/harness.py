@@ -93,7 +93,7 @@ class AttnProblem:
     def run_local(self, n_sink, window, out=None, lse=None):
         if out is None:
             out, lse = self.new_out(np.nan)
-        ws = torch.empty(self.P.attn_workspace_size(self.shape, n_sink, window), dtype=torch.uint8, device="cuda")
+        ws = torch.zeros(self.P.attn_workspace_size(self.shape, n_sink, window), dtype=torch.uint8, device="cuda")
         self.P.local_decode_attn(self.shape, self.inp, n_sink, window, out, lse, ws)
         torch.cuda.synchronize()
         return out, lse
@@ -101,7 +101,7 @@ class AttnProblem:
     def run_full(self, native_window=0, flags=None, work_list=None, n_work=None, out=None, lse=None):
         if out is None:
             out, lse = self.new_out(np.nan)
-        ws = torch.empty(self.P.attn_workspace_size(self.shape, 0, native_window), dtype=torch.uint8,
+        ws = torch.zeros(self.P.attn_workspace_size(self.shape, 0, native_window), dtype=torch.uint8,
                          device="cuda")
         self.P.full_decode_attn(self.shape, self.inp, native_window, flags, work_list, n_work, out, lse, ws)
         torch.cuda.synchronize()

@@ -155,3 +155,40 @@ def test_nan_in_unattended_slots_is_ignored():
                 p.v[:, p.table[b][0], :, :, pos] = nanbits
     p.upload()
     _cmp(p, p.run_local(4, 8), p.oracle_local(4, 8))
+
+
+@pytest.mark.parametrize("cur", [False, True])
+def test_one_workspace_serves_many_calls(cur):
+    """Split-K partials are merged by the last split of each request in the
+    same launch, counting with ticket words at the front of the workspace.
+    One zero-filled workspace, reused by Local and Full calls with different
+    windows and selections, gives results bit-identical to fresh workspaces,
+    matches the oracle, and is left with every ticket word zero."""
+    pb = AttnProblem(41, 3, 4, 16, 4, 64, [300, 77, 513, 160], cur=cur, split_blocks=2)
+    P = pb.P
+    sizes = [P.attn_workspace_size(pb.shape, s, w) for s, w in ((4, 64), (0, 32), (0, 0))]
+    ws = torch.zeros(max(sizes), dtype=torch.uint8, device="cuda")
+    wl, nw = dev_i32([3, 0, 2, 1]), dev_i32([3])
+    calls = [("local", 4, 64, None), ("full", 0, 0, None), ("local", 0, 32, None), ("full", 0, 0, (wl, nw)),
+             ("local", 4, 64, None)]
+    for kind, s, w, sel in calls:
+        out, lse = pb.new_out(7.0)
+        ref_out, ref_lse = pb.new_out(7.0)
+        if kind == "local":
+            P.local_decode_attn(pb.shape, pb.inp, s, w, out, lse, ws)
+            pb.run_local(s, w, ref_out, ref_lse)
+            want = pb.oracle_local(s, w)
+        else:
+            args = (None, *sel) if sel else (None, None, None)
+            P.full_decode_attn(pb.shape, pb.inp, 0, *args, out, lse, ws)
+            pb.run_full(0, *args, out=ref_out, lse=ref_lse)
+            want = pb.oracle_full(requests=[3, 0, 2] if sel else None)
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref_out) and torch.equal(lse, ref_lse)
+        rows = [3, 0, 2] if sel else range(pb.B)
+        o = out.cpu().numpy()
+        check_close(o[:, rows], want[0][:, rows])
+        if sel:
+            assert np.all(o[:, 1] == 7.0)
+        units = pb.L * pb.B * pb.Hkv
+        assert int(ws[:4 * units].view(torch.int32).abs().sum().item()) == 0

@@ -44,8 +44,8 @@ def test_decode_loop_with_commit(D, G):
     gate = P.gate_desc(P.HEAD_MLP, d, 16, dev_f32(params))
     dh, de, dhl = dev_f32(h), dev_f32(e), dev_f32(hl)
     shape = P.Shape(L, B, Hq, Hkv, D, mb, int(seq0.max()) + T, nb, 2)
-    ws_l = torch.empty(max(1, P.attn_workspace_size(shape, s, W)), dtype=torch.uint8, device="cuda")
-    ws_f = torch.empty(max(1, P.attn_workspace_size(shape, 0, 0)), dtype=torch.uint8, device="cuda")
+    ws_l = torch.zeros(max(1, P.attn_workspace_size(shape, s, W)), dtype=torch.uint8, device="cuda")
+    ws_f = torch.zeros(max(1, P.attn_workspace_size(shape, 0, 0)), dtype=torch.uint8, device="cuda")
     ws_g = torch.empty(P.gate_workspace_size(gate, B), dtype=torch.uint8, device="cuda")
     score = torch.empty(B, device="cuda")
     flags = torch.empty(B, dtype=torch.int32, device="cuda")

@@ -37,8 +37,8 @@ def test_graph_replay_matches_eager():
     dtab = dev_i32(table)
     seq_init = dev_i32(seq0)
     dseq = seq_init.clone()
-    ws_l = torch.empty(max(256, P.attn_workspace_size(shape, s, W)), dtype=torch.uint8, device="cuda")
-    ws_f = torch.empty(max(256, P.attn_workspace_size(shape, 0, 0)), dtype=torch.uint8, device="cuda")
+    ws_l = torch.zeros(max(256, P.attn_workspace_size(shape, s, W)), dtype=torch.uint8, device="cuda")
+    ws_f = torch.zeros(max(256, P.attn_workspace_size(shape, 0, 0)), dtype=torch.uint8, device="cuda")
     ws_g = torch.empty(P.gate_workspace_size(gate, B), dtype=torch.uint8, device="cuda")
     score = torch.empty(B, device="cuda")
     flags = torch.empty(B, dtype=torch.int32, device="cuda")
