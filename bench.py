@@ -174,7 +174,7 @@ class Bench:
         params = S.gate_params(self.seed, head, wl.d_model, wl.d_hidden)
         self.params = torch.from_numpy(params).to(self.dev)
         self.gate = P.gate_desc(kind, wl.d_model, wl.d_hidden, self.params, 1e-6)
-        self.ws_gate = torch.empty(P.gate_workspace_size(self.gate, wl.batch), dtype=torch.uint8, device=self.dev)
+        self.ws_gate = torch.zeros(P.gate_workspace_size(self.gate, wl.batch), dtype=torch.uint8, device=self.dev)
 
     # -- calls ---------------------------------------------------------------
     def step_calls(self, tau, forced=None, gated_only=False):

@@ -100,7 +100,7 @@ class Decoder:
         self.counter = torch.zeros(1, dtype=torch.int64, device=dev)
         self.gate, self.tau = gate, tau
         self.forced = torch.zeros(B, **i32) if prescribed else None
-        self.ws_gate = None if gate is None else torch.empty(P.gate_workspace_size(gate, B), dtype=torch.uint8,
+        self.ws_gate = None if gate is None else torch.zeros(P.gate_workspace_size(gate, B), dtype=torch.uint8,
                                                              device=dev)
         # one-layer attention calls: the layer's slices of the caches and candidates
         self.attn_shape = P.Shape(1, B, Hq, Hkv, D, max_blocks_per_seq, max_seq_len, num_blocks, split_blocks)

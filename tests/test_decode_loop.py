@@ -46,7 +46,7 @@ def test_decode_loop_with_commit(D, G):
     shape = P.Shape(L, B, Hq, Hkv, D, mb, int(seq0.max()) + T, nb, 2)
     ws_l = torch.zeros(max(1, P.attn_workspace_size(shape, s, W)), dtype=torch.uint8, device="cuda")
     ws_f = torch.zeros(max(1, P.attn_workspace_size(shape, 0, 0)), dtype=torch.uint8, device="cuda")
-    ws_g = torch.empty(P.gate_workspace_size(gate, B), dtype=torch.uint8, device="cuda")
+    ws_g = torch.zeros(P.gate_workspace_size(gate, B), dtype=torch.uint8, device="cuda")
     score = torch.empty(B, device="cuda")
     flags = torch.empty(B, dtype=torch.int32, device="cuda")
     wl = torch.empty(B, dtype=torch.int32, device="cuda")

@@ -24,7 +24,7 @@ class Gate:
         self.dparams = dev_f32(self.params)
         self.desc = self.P.gate_desc(self.P.HEAD_PAPER if kind == "paper" else self.P.HEAD_MLP, d, dh,
                                      self.dparams, eps)
-        self.ws = torch.empty(self.P.gate_workspace_size(self.desc, batch), dtype=torch.uint8, device="cuda")
+        self.ws = torch.zeros(self.P.gate_workspace_size(self.desc, batch), dtype=torch.uint8, device="cuda")
         self.counter = torch.zeros(1, dtype=torch.int64, device="cuda")
 
     def run(self, h, e, l, tau, forced=None):

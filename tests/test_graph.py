@@ -39,7 +39,7 @@ def test_graph_replay_matches_eager():
     dseq = seq_init.clone()
     ws_l = torch.zeros(max(256, P.attn_workspace_size(shape, s, W)), dtype=torch.uint8, device="cuda")
     ws_f = torch.zeros(max(256, P.attn_workspace_size(shape, 0, 0)), dtype=torch.uint8, device="cuda")
-    ws_g = torch.empty(P.gate_workspace_size(gate, B), dtype=torch.uint8, device="cuda")
+    ws_g = torch.zeros(P.gate_workspace_size(gate, B), dtype=torch.uint8, device="cuda")
     score = torch.empty(B, device="cuda")
     flags = torch.empty(B, dtype=torch.int32, device="cuda")
     wl = torch.empty(B, dtype=torch.int32, device="cuda")

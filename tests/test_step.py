@@ -19,7 +19,7 @@ def _step(p, g, gate_kind, d, dh, h, e, l, tau, s=4, W=24, forced=None):
     out, lse = p.new_out(np.nan)
     ws_l = torch.zeros(P.attn_workspace_size(p.shape, s, W), dtype=torch.uint8, device="cuda")
     ws_f = torch.zeros(P.attn_workspace_size(p.shape, 0, 0), dtype=torch.uint8, device="cuda")
-    ws_g = torch.empty(P.gate_workspace_size(g, B), dtype=torch.uint8, device="cuda")
+    ws_g = torch.zeros(P.gate_workspace_size(g, B), dtype=torch.uint8, device="cuda")
     score = torch.empty(B, dtype=torch.float32, device="cuda")
     flags = torch.empty(B, dtype=torch.int32, device="cuda")
     wl = torch.empty(B, dtype=torch.int32, device="cuda")
