@@ -365,9 +365,10 @@ class Bench:
                 self._layers.append((st, sh, ws_l, ws_f, ins))
         return self._layers
 
-    def per_layer_calls(self, tau, forced):
+    def per_layer_calls(self, tau, forced, split=False):
         """One decode step as one call per layer: every layer's Local, the gate
-        (reading the staged inputs), every layer's Full over the compacted list."""
+        (reading the staged inputs), every layer's Full over the compacted list
+        (split: the Local + gate calls and the Full calls as two lists)."""
         P = self.P
         calls = []
         for st, sh, ws_l, _, ins in self._layer_state():
@@ -376,15 +377,19 @@ class Bench:
         calls.append(P.prepare_gate(self.gate, self.wl.batch, self.h_stage, self.e_stage, self.l_stage, tau,
                                     self.f_stage if forced is not None else None, self.score, self.flags,
                                     self.work, self.n_work, self.counter, self.ws_gate))
+        full = []
         for st, sh, _, ws_f, ins in self._layer_state():
-            calls += [P.prepare_full(sh, inp, st.stack.native_window, None, self.work, self.n_work, st.out[l],
-                                     st.lse[l], ws_f) for l, inp in enumerate(ins)]
-        return calls
+            full += [P.prepare_full(sh, inp, st.stack.native_window, None, self.work, self.n_work, st.out[l],
+                                    st.lse[l], ws_f) for l, inp in enumerate(ins)]
+        return (calls, full) if split else calls + full
 
     def per_layer(self, tau, forced, warmup):
         """Per-layer launches of the K steps, eager and replayed as one captured
         HIP graph per step shape (gate inputs staged before each step, outside
-        the events).  Returns (eager, graph) timing dicts."""
+        the events), and eager with a host branch: the Full calls are launched
+        only if the host, after one synchronisation on the device's count of
+        flagged requests, sees any (the branch of Alg. 1).  Returns (eager,
+        graph, host-branch) timing dicts."""
         torch = self.torch
         K = self.K
 
@@ -404,7 +409,17 @@ class Bench:
                 c()
         graph = self.timed([[g.replay]] * K, warmup, cold=True, pre=pre)
         del g
-        return eager, graph
+        first, full = self.per_layer_calls(tau, forced, split=True)
+        n_host = torch.zeros(1, dtype=torch.int32).pin_memory()
+
+        def branch():
+            n_host.copy_(self.n_work, non_blocking=True)
+            torch.cuda.current_stream().synchronize()
+            if int(n_host[0]) > 0:
+                for c in full:
+                    c()
+        branched = self.timed([first + [branch]] * K, warmup, cold=True, pre=pre)
+        return eager, graph, branched
 
     def per_layer_full(self, warmup):
         """Always-Full in the per-layer launch mode: one Full call per layer over
@@ -742,14 +757,16 @@ def run_per_layer(b, wl, args, points):
     log(f"[bench] per-layer always-Full: eager {fe['us_mean']:.1f} us/step, graph {fg['us_mean']:.1f} us/step")
     out = []
     for pt in points:
-        eager, graph = b.per_layer(pt["tau"], pt["forced"], args.warmup)
+        eager, graph, branched = b.per_layer(pt["tau"], pt["forced"], args.warmup)
         ent = dict(mode=pt["mode"], rho=pt["rho"], realised_rho=eager["recalled"] / (b.K * wl.batch),
-                   eager_us=eager["us_mean"], graph_us=graph["us_mean"],
+                   eager_us=eager["us_mean"], graph_us=graph["us_mean"], host_branch_us=branched["us_mean"],
                    graph_realised_rho=graph["recalled"] / (b.K * wl.batch),
-                   eager_ratio=eager["us_mean"] / fe["us_mean"], graph_ratio=graph["us_mean"] / fg["us_mean"])
+                   eager_ratio=eager["us_mean"] / fe["us_mean"], graph_ratio=graph["us_mean"] / fg["us_mean"],
+                   host_branch_ratio=branched["us_mean"] / fe["us_mean"])
         out.append(ent)
         log(f"[bench] per-layer launches rho={pt['rho']:.3f}: eager {eager['us_mean']:.1f} us/step, "
-            f"graph {graph['us_mean']:.1f} us/step (x{ent['eager_ratio']:.3f} of per-layer always-Full)")
+            f"graph {graph['us_mean']:.1f}, host branch {branched['us_mean']:.1f} "
+            f"(x{ent['eager_ratio']:.3f} / x{ent['host_branch_ratio']:.3f} of per-layer always-Full)")
     return base, out
 
 
