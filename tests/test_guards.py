@@ -110,3 +110,15 @@ def test_dense_and_row_copy_skip_listed_requests_outside_the_batch():
     torch.cuda.synchronize()
     d = dst.cpu().numpy()
     assert np.all(d[1] == np.arange(8, 16)) and np.all(d[[0, 2]] == -1.0)
+
+
+def test_stream_read_reads_and_leaves_the_sink():
+    """The read-ceiling aid reads any 16-byte multiple and writes nothing
+    (its sink keeps its value unless the XOR of the data hits one constant)."""
+    P = need_gpu()
+    x = torch.arange(1 << 20, dtype=torch.int32, device="cuda")
+    sink = torch.full((1,), 12345, dtype=torch.int32, device="cuda")
+    for nbytes, groups in ((x.numel() * 4, 0), (4096 + 16, 3), (16, 1), (x.numel() * 4, 1000)):
+        P.stream_read(x, nbytes, sink, groups)
+    torch.cuda.synchronize()
+    assert int(sink.item()) == 12345
