@@ -98,21 +98,34 @@ def test_llama_full_size():
     for tau in (math.inf, -math.inf):
         _run_step(b, tau)
         flags = _check_gate(b, tau)
-        _check_rows(b, flags, [(0, 0, 0), (0, 17, 0), (0, 31, 0)])
+        _check_rows(b, flags, [(0, 0, 0), (0, 16, 0), (0, 31, 0)])
+
+
+def _sampled_requests(b, flags, k, seed):
+    """k seeded requests, always including a flagged and an unflagged one."""
+    rng = np.random.default_rng(seed)
+    on, off = np.flatnonzero(flags), np.flatnonzero(~flags)
+    pick = {int(on[0]), int(off[0])} if len(on) and len(off) else set()
+    for r in rng.permutation(b.wl.batch):
+        if len(pick) >= k:
+            break
+        pick.add(int(r))
+    return sorted(pick)
 
 
 def test_long_full_size():
+    """Layers {0, L/2, L-1} x every request (the four 131,072-position ones)."""
     b = _bench("long")
     tau = _median_tau(b)
     _run_step(b, tau)
     flags = _check_gate(b, tau)
     assert 0 < flags.sum() < b.wl.batch
-    on = int(np.flatnonzero(flags)[0])
-    off = int(np.flatnonzero(~flags)[0])
-    _check_rows(b, flags, [(0, 0, on), (0, 31, off), (0, 13, on)])
+    _check_rows(b, flags, [(0, l, r) for l in (0, 16, 31) for r in range(b.wl.batch)])
 
 
 def test_mixed_full_size():
+    """Layers {0, L/2, L-1} x four seeded requests, plus the longest flagged
+    and the shortest unflagged request."""
     b = _bench("mixed")
     tau = _median_tau(b)
     _run_step(b, tau)
@@ -122,18 +135,25 @@ def test_mixed_full_size():
     lens = b.seq_host
     longest_on = int(on[np.argmax(lens[on])])
     shortest_off = int(off[np.argmin(lens[off])])
-    _check_rows(b, flags, [(0, 0, longest_on), (0, 31, shortest_off), (0, 5, int(on[0]))])
+    reqs = _sampled_requests(b, flags, 4, 7)
+    _check_rows(b, flags, [(0, l, r) for l in (0, 16, 31) for r in reqs]
+                + [(0, 5, longest_on), (0, 27, shortest_off)])
 
 
 def test_hybrid_full_size():
+    """Both layer groups (stack 0: native sliding-window layers; stack 1:
+    global, ODA-gated layers) at their first, middle and last layer x four
+    seeded requests."""
     b = _bench("hybrid")
     tau = _median_tau(b)
     _run_step(b, tau)
     flags = _check_gate(b, tau)
-    on = int(np.flatnonzero(flags)[0])
-    off = int(np.flatnonzero(~flags)[0])
-    # stack 0: native sliding-window layers; stack 1: global, ODA-gated layers
-    _check_rows(b, flags, [(0, 0, off), (0, 35, on), (1, 0, on), (1, 11, off)])
+    reqs = _sampled_requests(b, flags, 4, 8)
+    rows = []
+    for si, st in enumerate(b.stacks):
+        L = st.stack.num_layers
+        rows += [(si, l, r) for l in (0, L // 2, L - 1) for r in reqs]
+    _check_rows(b, flags, rows)
 
 
 def test_llama_per_layer_launches_eager_and_graph():
