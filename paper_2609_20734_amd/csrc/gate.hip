@@ -113,6 +113,14 @@ __global__ __launch_bounds__(256) void gate_linear_kernel(LinArgs p) {
   }
   const float* wrow = W + (int64_t)row0 * p.K;
   const float* wrow2 = kTwo ? p.W2 + (int64_t)row0 * p.K : nullptr;
+  // the epilogue's bias or residual for the output this lane will hold (lane
+  // j * 8 + bi: row j, request bi), read now so it is not a dependent load
+  // after the reduction; clamped to a valid element for lanes without one
+  float epi = 0.f;
+  if (MODE != kGateUp) {
+    const int ej = min(lane / kBatchTile, R - 1), eb = b0 + min(lane % kBatchTile, nb - 1);
+    epi = MODE == kDown ? p.aux[(int64_t)eb * p.rows + row0 + ej] : bias[row0 + ej];
+  }
 
   float acc[R][kBatchTile], acc2[kTwo ? R : 1][kBatchTile], ss[kBatchTile];
 #pragma unroll
@@ -207,13 +215,13 @@ __global__ __launch_bounds__(256) void gate_linear_kernel(LinArgs p) {
   const int row = row0 + j;
   const float inv = kNorm ? rsqrtf(my_ss / (float)p.K + p.eps) : 1.f;
   if (MODE == kTower) {
-    p.Y[((int64_t)tower * p.B + b) * p.dt + row] = silu(v * inv + bias[row]);
+    p.Y[((int64_t)tower * p.B + b) * p.dt + row] = silu(v * inv + epi);
   } else if (MODE == kMlpHidden) {
-    p.Y[(int64_t)b * p.rows + row] = gelu(v + bias[row]);
+    p.Y[(int64_t)b * p.rows + row] = gelu(v + epi);
   } else if (MODE == kGateUp) {
     p.Y[(int64_t)b * p.rows + row] = silu(v * inv) * (v2 * inv);
   } else {  // kDown
-    p.Y[(int64_t)b * p.rows + row] = p.aux[(int64_t)b * p.rows + row] + v;
+    p.Y[(int64_t)b * p.rows + row] = epi + v;
   }
 }
 
@@ -240,6 +248,15 @@ __global__ __launch_bounds__(256) void gate_fusion_kernel(LinArgs p) {
   const int dt = p.dt;
   const float* wrow = p.W + (int64_t)row * 9 * dt;
   const float* abc = p.aux;
+  // the epilogue's operands for request b0 + lane (a + b + c at this row and
+  // the bias), read before the main loop; clamped for lanes without one
+  float s3 = 0.f, brow = 0.f;
+  if (valid) {
+    const int eb = b0 + min(lane, nb - 1);
+    s3 = abc[((int64_t)0 * p.B + eb) * dt + row] + abc[((int64_t)1 * p.B + eb) * dt + row] +
+         abc[((int64_t)2 * p.B + eb) * dt + row];
+    brow = p.bias[row];
+  }
   float acc[kBatchTile];
 #pragma unroll
   for (int bi = 0; bi < kBatchTile; ++bi) acc[bi] = 0.f;
@@ -279,9 +296,7 @@ __global__ __launch_bounds__(256) void gate_fusion_kernel(LinArgs p) {
   }
   if (lane >= nb) return;
   const int b = b0 + lane;
-  const float s3 = abc[((int64_t)0 * p.B + b) * dt + row] + abc[((int64_t)1 * p.B + b) * dt + row] +
-                   abc[((int64_t)2 * p.B + b) * dt + row];
-  p.Y[(int64_t)b * p.rows + row] = 0.5f * (s3 + silu(mine + p.bias[row]));
+  p.Y[(int64_t)b * p.rows + row] = 0.5f * (s3 + silu(mine + brow));
 }
 
 constexpr int kSplitMaxB = 2;         // batches up to this size may take the split-hidden blocks
@@ -361,6 +376,17 @@ __global__ __launch_bounds__(kFinalWaves * 64) void gate_final_kernel(FinalArgs 
   const int lane = threadIdx.x & 63;
   const int wave = uniform(threadIdx.x >> 6);
   const bool norm = p.gain != nullptr;
+  // the projection w (times the gain) of this lane's first two 256-wide
+  // chunks, loaded before the input so its latency overlaps the gathering
+  constexpr int kPre = 2;
+  float4 wpre[kPre];
+#pragma unroll
+  for (int c = 0; c < kPre; ++c) {
+    const int k = 4 * lane + 256 * c;
+    const bool in = k < p.K;
+    wpre[c] = load4_or_zero(p.w + k, p.w, in);
+    if (norm) wpre[c] = mul4(wpre[c], load4_or_zero(p.gain + k, p.gain, in));
+  }
   // split-hidden blocks (B <= kSplitMaxB): z = residual + the last block's
   // partial sums, formed once in LDS by the whole workgroup
   const bool parts = p.parts != nullptr;
@@ -372,7 +398,16 @@ __global__ __launch_bounds__(kFinalWaves * 64) void gate_final_kernel(FinalArgs 
     for (int i = wave; i < nc; i += kFinalWaves) {
       const int b = c0 + i;
       float dot = 0.f, ss = 0.f;
-      for (int k = 4 * lane; k < p.K; k += 256) {
+#pragma unroll
+      for (int c = 0; c < kPre; ++c) {
+        const int k = 4 * lane + 256 * c;
+        if (k < p.K) {
+          const float4 x = *reinterpret_cast<const float4*>(X + (int64_t)b * p.K + k);
+          if (norm) ss += dot4(x, x);
+          dot += dot4(wpre[c], x);
+        }
+      }
+      for (int k = 4 * lane + 256 * kPre; k < p.K; k += 256) {
         const float4 x = *reinterpret_cast<const float4*>(X + (int64_t)b * p.K + k);
         float4 wk = *reinterpret_cast<const float4*>(p.w + k);
         if (norm) {
