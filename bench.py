@@ -718,9 +718,13 @@ def step_bytes(wl, b, pt, recalled, gated_only=False):
 def run_sweep(b, wl, args, full_us, gated_only=False, points=None):
     """Time the step at every operating point: `reps` repetitions of the K
     cold steps (the value is the median of the repetitions' means), then the
-    same K steps warm (back to back, no flush)."""
+    same K steps warm (back to back, no flush).  The always-Full step is timed
+    again after every point, and each point's ratio uses the mean of the
+    always-Full times just before and just after it, so that drift of the
+    box's speed during a long run cancels."""
     K = b.K
     sweep = []
+    full_before = full_us
     for pt in (points if points is not None else sweep_points(b, wl, args)):
         calls = b.step_calls(pt["tau"], forced=pt["forced"], gated_only=gated_only)
         reps = [b.timed(calls, args.warmup if i == 0 else 2, cold=True) for i in range(args.reps)]
@@ -730,10 +734,13 @@ def run_sweep(b, wl, args, full_us, gated_only=False, points=None):
         recalled = reps[0]["recalled"]
         real = recalled / (K * wl.batch)
         nbytes, bytes_full = step_bytes(wl, b, pt, recalled, gated_only)
+        full_after = b.timed(b.full_calls(), 2, cold=True)["us_mean"]
+        full_adj = 0.5 * (full_before + full_after)
+        full_before = full_after
         ent = dict(mode=pt["mode"], rho=pt["rho"], realised_rho=real, us=us, us_rep_min=min(means),
                    us_rep_max=max(means), us_step_median=float(np.median(per)), us_step_min=float(per.min()),
-                   us_step_max=float(per.max()), GBps=nbytes / us / 1e3, ratio=us / full_us,
-                   ideal_ratio=nbytes / bytes_full)
+                   us_step_max=float(per.max()), GBps=nbytes / us / 1e3, full_adjacent_us=full_adj,
+                   ratio=us / full_adj, ratio_first_full=us / full_us, ideal_ratio=nbytes / bytes_full)
         if pt["mode"] == "tau":
             ent["tau"] = pt["tau"]
         ent["hbm_frac"] = ent["GBps"] / HBM_PEAK_GBS
