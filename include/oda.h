@@ -195,7 +195,8 @@ oda_status oda_recall_gate(const oda_gate_desc *gate, int32_t batch, const float
  * sliding-window layers, which ODA leaves unrestricted).
  * Request selection:
  *   work_list != NULL (with n_work != NULL): exactly the listed requests
- *                       (work_list[0 .. *n_work-1]);
+ *                       (work_list[0 .. *n_work-1], distinct, as
+ *                       oda_recall_gate writes them);
  *   else flags != NULL: the requests with flags[b] != 0;
  *   else              : every request.
  * Only selected requests read KV; only their rows of out (and lse, if not
