@@ -41,3 +41,40 @@ def test_llama_config_sizes():
     assert full["kv"] == 32 * 8 * 32768 * 4 * 128 == 4_294_967_296
     loc = PL.attention_bytes(wl.seq_lens, 4, 1024, 32, 32, 8, 128)
     assert loc["kv"] == 32 * 8 * 1028 * 512
+
+
+def _kv(wl, seq, stacks, local):
+    tot = 0
+    for st in stacks:
+        if local:
+            s, w = (st.local_sink, st.local_window) if st.gated else (0, st.native_window)
+        else:
+            s, w = 0, st.native_window
+        tot += PL.attention_bytes(seq, s, w, st.num_layers, wl.num_q_heads, wl.num_kv_heads, wl.head_dim)["kv"]
+    return tot
+
+
+@pytest.mark.parametrize("name,rhos,want,gated_only", [
+    ("llama3-8b", (0, .1, .25, .5, 1), (0.032, 0.132, 0.282, 0.532, 1.032), False),
+    ("long", (0, .05, .2, 1), (0.031, 0.081, 0.231, 1.031), False),
+    ("hybrid", (0, .1, .25, .5, 1), (0.211, 0.311, 0.461, 0.711, 1.211), False),
+    ("hybrid", (0, .1, .25, .5, 1), (0.211, 0.295, 0.422, 0.632, 1.053), True)])
+def test_ideal_ratios_match_independent_ledger(name, rhos, want, gated_only):
+    """Ideal bytes ratios (KV + MLP-head weights) of the measured
+    configurations, computed independently from the configuration sizes:
+    Bytes(rho) / Bytes_Full with the retry over every layer, or over the gated
+    layers only.  The bench's own ratio (which also counts q, out, lse and
+    block tables) stays within 0.001 of them."""
+    import bench as BN
+    wl = WL.ALL[name]
+    seq = np.array(wl.seq_lens)
+    full = _kv(wl, seq, wl.stacks, False)
+    local = _kv(wl, seq, wl.stacks, True)
+    retry = _kv(wl, seq, [st for st in wl.stacks if st.gated or not gated_only], False)
+    gate = PL.gate_bytes("mlp", wl.batch, wl.d_model, wl.d_hidden)["weights"]
+    for rho, w in zip(rhos, want):
+        assert round((local + gate + rho * retry) / full, 3) == w
+        lb, gb, fb = BN.bytes_for(wl, seq, None, "mlp", gated_only)
+        _, _, fall = BN.bytes_for(wl, seq, None, "mlp")
+        bench_ratio = (lb + gb + rho * sum(fb)) / sum(fall)
+        assert abs(bench_ratio - (local + gate + rho * retry) / full) < 1e-3
