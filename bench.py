@@ -721,7 +721,7 @@ def run_sweep(b, wl, args, full_us, gated_only=False, points=None):
     same K steps warm (back to back, no flush).  The always-Full step is timed
     again after every point, and each point's ratio uses the mean of the
     always-Full times just before and just after it, so that drift of the
-    box's speed during a long run cancels."""
+    machine's speed during a long run cancels."""
     K = b.K
     sweep = []
     full_before = full_us
