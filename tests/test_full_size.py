@@ -199,3 +199,23 @@ def test_hybrid_retry_on_gated_layers_only():
     on = int(np.flatnonzero(flags)[0])
     off = int(np.flatnonzero(~flags)[0])
     _check_rows(b, flags, [(0, 3, on), (0, 20, off), (1, 2, on), (1, 7, off)])
+
+
+def test_hybrid_per_layer_launches():
+    """Per-layer launches over both layer groups (natively windowed layers and
+    gated global layers, one call per layer each) against the oracle."""
+    b = _bench("hybrid")
+    tau = _median_tau(b)
+    b.h_stage.copy_(b.h[0])
+    b.e_stage.copy_(b.e[0])
+    b.l_stage.copy_(b.l[0])
+    for c in b.per_layer_calls(tau, None):
+        c()
+    torch.cuda.synchronize()
+    flags = _check_gate(b, tau)
+    reqs = _sampled_requests(b, flags, 3, 9)
+    rows = []
+    for si, st in enumerate(b.stacks):
+        L = st.stack.num_layers
+        rows += [(si, l, r) for l in (1, L - 2) for r in reqs]
+    _check_rows(b, flags, rows)
