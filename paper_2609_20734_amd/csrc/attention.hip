@@ -711,7 +711,9 @@ oda_status check_shape(const oda_attn_shape* s) {
 // requests to give the GPU about ODA_TARGET_GROUPS workgroups (one per CU):
 // the grid and the workspace are sized for the case of a single selected
 // request (max_splits); the kernels pick the actual split count on the device
-// (effective_bps), so most calls finish in the split kernel.
+// (effective_bps).  A request covered by one split is finalised by its
+// workgroup; otherwise the last of its splits merges them in the same launch.
+// Workspace: the ticket words (one per unit), then the partial o, then (m, l).
 void make_plan(const oda_attn_shape* s, int n_sink, int window, Plan* p) {
   const int64_t total_blocks = oda::ceil_div(s->max_seq_len, kBlock);
   int64_t nvb = total_blocks;
