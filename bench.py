@@ -724,7 +724,7 @@ def run_sweep(b, wl, args, full_us, gated_only=False, points=None):
     machine's speed during a long run cancels."""
     K = b.K
     sweep = []
-    full_before = full_us
+    full_before = getattr(b, "last_full_us", full_us)
     for pt in (points if points is not None else sweep_points(b, wl, args)):
         calls = b.step_calls(pt["tau"], forced=pt["forced"], gated_only=gated_only)
         reps = [b.timed(calls, args.warmup if i == 0 else 2, cold=True) for i in range(args.reps)]
@@ -736,7 +736,7 @@ def run_sweep(b, wl, args, full_us, gated_only=False, points=None):
         nbytes, bytes_full = step_bytes(wl, b, pt, recalled, gated_only)
         full_after = b.timed(b.full_calls(), 2, cold=True)["us_mean"]
         full_adj = 0.5 * (full_before + full_after)
-        full_before = full_after
+        full_before = b.last_full_us = full_after
         ent = dict(mode=pt["mode"], rho=pt["rho"], realised_rho=real, us=us, us_rep_min=min(means),
                    us_rep_max=max(means), us_step_median=float(np.median(per)), us_step_min=float(per.min()),
                    us_step_max=float(per.max()), GBps=nbytes / us / 1e3, full_adjacent_us=full_adj,
