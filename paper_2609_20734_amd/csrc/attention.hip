@@ -64,6 +64,8 @@ constexpr int kBlock = 16;            // positions per KV block
 constexpr int kMaxGroup = 16;         // query heads per KV head held by one MFMA tile
 constexpr int kWaves = ODA_SPLIT_WAVES;   // wavefronts per split workgroup
 constexpr int kMergeThreads = 256;
+constexpr int kMergeChunk = 16;       // split partials read per round trip in the merge
+constexpr int kMergeSmall = 4;        // chunk used for the last few splits
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -159,22 +161,53 @@ __device__ __forceinline__ bool resolve_request(const AttnArgs& a, int slot, int
 
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
+// Requests with work in this call: the work list's count (at most the batch),
+// the number of set flags, or the whole batch.  Uniform over the wavefront.
+__device__ __forceinline__ int active_requests(const AttnArgs& a) {
+  if (a.select == kSelList) return uniform(min(max(a.n_work[0], 0), a.B));
+  if (a.select != kSelFlags) return a.B;
+  int active = 0;
+  for (int b0 = 0; b0 < a.B; b0 += 64) {
+    const int b = b0 + (int)(threadIdx.x & 63);
+    active += __popcll(__ballot(b < a.B && a.flags[b] != 0));
+  }
+  return uniform(active);
+}
+
+// The request of the rank-th active slot (ascending request order for flags,
+// list order for a work list); false if the listed id is outside the batch.
+__device__ __forceinline__ bool request_of_rank(const AttnArgs& a, int rank, int& b) {
+  if (a.select == kSelList) {
+    b = a.work_list[rank];
+    return b >= 0 && b < a.B;
+  }
+  if (a.select != kSelFlags) {
+    b = rank;
+    return true;
+  }
+  const int lane = (int)(threadIdx.x & 63);
+  int seen = 0;
+  for (int b0 = 0; b0 < a.B; b0 += 64) {
+    const uint64_t m = __ballot(b0 + lane < a.B && a.flags[b0 + lane] != 0);
+    const int c = __popcll(m);
+    if (rank < seen + c) {
+      // the lane whose flag is set with exactly rank - seen set flags below it
+      const uint64_t below = m & ((1ull << lane) - 1ull);
+      const bool hit = ((m >> lane) & 1ull) != 0 && __popcll(below) == rank - seen;
+      b = b0 + __builtin_ctzll(__ballot(hit));
+      return true;
+    }
+    seen += c;
+  }
+  return false;
+}
+
 // Blocks per split for this call.  With the automatic plan the split count
 // depends on how many requests are selected (known only on the device for
 // Full): enough splits that the selected requests give about
 // ODA_TARGET_GROUPS workgroups, at most max_splits (sized for one request).
-__device__ __forceinline__ int effective_bps(const AttnArgs& a) {
+__device__ __forceinline__ int effective_bps(const AttnArgs& a, int active) {
   if (!a.dyn_splits) return a.bps;
-  int active = a.B;
-  if (a.select == kSelList) {
-    active = a.n_work[0];
-  } else if (a.select == kSelFlags) {
-    active = 0;
-    for (int b0 = 0; b0 < a.B; b0 += 64) {
-      const int b = b0 + (int)(threadIdx.x & 63);
-      active += __popcll(__ballot(b < a.B && a.flags[b] != 0));
-    }
-  }
   const int64_t units = (int64_t)max(active, 1) * a.L * a.Hkv;
   const int64_t want = (ODA_TARGET_GROUPS + units - 1) / units;
   const int s = (int)max((int64_t)1, min((int64_t)a.max_splits, want));
@@ -373,6 +406,40 @@ __host__ __device__ constexpr size_t split_lds_floats(int G, int D) {
   return (size_t)kWaves * 32 + (size_t)kWaves * G * D + 16;
 }
 
+// Running state of one output element of the split merge: maximum logit M
+// (log2 units), weighted sum of partial outputs and of partial denominators.
+struct MergeAcc {
+  float M = -INFINITY, acc = 0.f, lam = 0.f;
+};
+
+// Fold splits [s0, s0 + C) of one (query head hh, dimension d) into m; indices
+// past the last split repeat it with weight 0.
+template <int C, int D>
+__device__ __forceinline__ void merge_chunk(MergeAcc& m, const float* ml, const float* po, int s0, int nsplit,
+                                            int G, int hh, int d) {
+  float mv[C], lv[C], ov[C];
+#pragma unroll
+  for (int k = 0; k < C; ++k) {
+    const int s = min(s0 + k, nsplit - 1);
+    mv[k] = ml[(s * G + hh) * 2];
+    lv[k] = ml[(s * G + hh) * 2 + 1];
+    ov[k] = po[((int64_t)s * G + hh) * D + d];
+  }
+  float Mc = m.M;
+#pragma unroll
+  for (int k = 0; k < C; ++k) Mc = fmaxf(Mc, mv[k]);
+  const float r = (Mc == m.M) ? 1.f : exp2_fast(m.M - Mc);
+  m.acc *= r;
+  m.lam *= r;
+  m.M = Mc;
+#pragma unroll
+  for (int k = 0; k < C; ++k) {
+    const float w = (s0 + k < nsplit) ? exp2_fast(mv[k] - Mc) : 0.f;
+    m.acc += w * ov[k];
+    m.lam += w * lv[k];
+  }
+}
+
 // Combine the nsplit partials of one (layer, request, KV head) with stable
 // softmax rescaling (plus the uncommitted candidate) and write out / lse.
 // Called by every thread of a workgroup of `nthreads` threads (it holds a
@@ -405,25 +472,29 @@ __device__ __forceinline__ void merge_unit(const AttnArgs& a, int l, int b, int 
   }
   __syncthreads();
 
+  // The partials were written back from other XCDs, so every read is a trip to
+  // memory: a chunk of splits is loaded with all its reads in flight at once,
+  // and the running maximum is rescaled once per chunk.
   for (int e = threadIdx.x; e < G * D; e += nthreads) {
     const int hh = e / D, d = e - hh * D;
-    float M = a.has_cur ? sm_zc[hh] : -INFINITY;
-    for (int s = 0; s < nsplit; ++s) M = fmaxf(M, ml[(s * G + hh) * 2]);
-    float acc = 0.f, lam = 0.f;
-#pragma unroll 4
-    for (int s = 0; s < nsplit; ++s) {
-      const float w = exp2_fast(ml[(s * G + hh) * 2] - M);
-      acc += w * po[((int64_t)s * G + hh) * D + d];
-      lam += w * ml[(s * G + hh) * 2 + 1];
+    MergeAcc m;
+    if (a.has_cur) {   // the candidate's weight is exp2(zc - M) = 1 at M = zc
+      m.M = sm_zc[hh];
+      m.acc = bf16_to_float(a.v_cur[coff + d]);
+      m.lam = 1.f;
     }
-    if (a.has_cur) {
-      const float w = exp2_fast(sm_zc[hh] - M);
-      acc += w * bf16_to_float(a.v_cur[coff + d]);
-      lam += w;
+    for (int s0 = 0; s0 < nsplit;) {
+      if (nsplit - s0 > 2 * kMergeSmall) {
+        merge_chunk<kMergeChunk, D>(m, ml, po, s0, nsplit, G, hh, d);
+        s0 += kMergeChunk;
+      } else {
+        merge_chunk<kMergeSmall, D>(m, ml, po, s0, nsplit, G, hh, d);
+        s0 += kMergeSmall;
+      }
     }
-    a.out[qoff + e] = acc / lam;
+    a.out[qoff + e] = m.acc / m.lam;
     if (d == 0 && a.lse != nullptr)
-      a.lse[((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G + hh] = (M + __log2f(lam)) * kLn2;
+      a.lse[((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G + hh] = (m.M + __log2f(m.lam)) * kLn2;
   }
 }
 
@@ -440,20 +511,22 @@ void attn_split_kernel(AttnArgs a) {
   const int h16 = lane & 15;
   const int j = lane >> 4;
 
-  // split outermost, then request slot: the items that have work (the splits in
-  // use, the selected requests of a work list) form a prefix of the grid, so
-  // the dispatcher places them first instead of interleaving them with
-  // workgroups that exit at once
+  // split outermost, then the rank of the request among those with work: the
+  // items that have work (the splits in use of the selected requests) form a
+  // prefix of the grid, so the dispatcher spreads them over the CUs first
+  // instead of interleaving them with workgroups that exit at once
+  const int active = active_requests(a);
+  if (active == 0) return;
   int64_t item = blockIdx.x;
   const int g = (int)(item % a.Hkv);
   item /= a.Hkv;
   const int l = (int)(item % a.L);
   item /= a.L;
-  const int slot = (int)(item % a.B);
-  const int split = (int)(item / a.B);
-  if (split >= a.max_splits) return;
+  const int rank = (int)(item % active);
+  if (item / active >= a.max_splits) return;
+  const int split = (int)(item / active);
   int b;
-  if (!resolve_request(a, slot, b)) return;
+  if (!request_of_rank(a, rank, b)) return;
   b = uniform(b);
   const int n = uniform(a.seq_lens[b]);
   const int G = a.G;
@@ -469,7 +542,7 @@ void attn_split_kernel(AttnArgs a) {
   }
   Run r;
   r.geo = geometry(n, kLocal ? a.n_sink : 0, a.window, a.has_cur);
-  const int bps = effective_bps(a);
+  const int bps = effective_bps(a, active);
   // (nvb = 0 happens only with the candidate as the sole position: one item, no blocks)
   const int nsplit = max(1, (r.geo.nvb + bps - 1) / bps);
   if (split >= nsplit) return;   // uniform over the workgroup: no barrier is skipped by part of it
@@ -662,7 +735,7 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(AttnArgs a) {
   const int n = uniform(a.seq_lens[b]);
   if (!valid_len(a, n)) return;   // the split kernel wrote NaN rows
   const Geometry geo = geometry(n, a.n_sink, a.window, a.has_cur);
-  const int bps = effective_bps(a);
+  const int bps = effective_bps(a, active_requests(a));
   const int nsplit = max(1, (geo.nvb + bps - 1) / bps);
   if (nsplit <= 1) return;   // finalized by the split kernel
   merge_unit<D>(a, l, b, g, nsplit, sm_zc, kMergeThreads);

@@ -96,6 +96,36 @@ def test_full_touches_only_selected_requests(mode):
             assert np.all(o[:, b] == -7.0) and np.all(lse.cpu().numpy()[:, b] == -7.0)
 
 
+@pytest.mark.parametrize("mode", ["flags", "list"])
+def test_few_selected_of_a_wide_batch(mode):
+    """A few selected requests of a 70-request batch (two 64-wide flag words),
+    one layer, automatic splits: the selected requests get several splits each
+    and the grid's leading workgroups map to them by rank (ascending ids for
+    flags, list order for a work list, here not ascending)."""
+    g = np.random.default_rng(70)
+    seq = g.integers(1, 400, size=70)
+    pick = [69, 3, 64]
+    seq[pick] = [1999, 1500, 777]
+    p = AttnProblem(70, 1, 70, 8, 2, 64, seq.tolist())
+    out, lse = p.new_out(-7.0)
+    if mode == "flags":
+        fl = np.zeros(70, np.int32)
+        fl[pick] = 1
+        p.run_full(0, flags=dev_i32(fl), out=out, lse=lse)
+    else:
+        wl = np.zeros(70, np.int32)
+        wl[:3] = pick
+        p.run_full(0, work_list=dev_i32(wl), n_work=dev_i32([3]), out=out, lse=lse)
+    o, ls = out.cpu().numpy(), lse.cpu().numpy()
+    ref = p.oracle_full(0, requests=pick)
+    for b in range(70):
+        if b in pick:
+            check_close(o[:, b], ref[0][:, b], what=f"request {b}")
+            assert np.max(np.abs(ls[:, b] - ref[1][:, b])) <= LSE_ABS
+        else:
+            assert np.all(o[:, b] == -7.0) and np.all(ls[:, b] == -7.0)
+
+
 def test_empty_work_list_writes_nothing():
     p = AttnProblem(2, 1, 3, 8, 2, 64, [10, 20, 30])
     out, lse = p.new_out(3.5)
