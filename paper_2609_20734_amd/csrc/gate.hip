@@ -161,8 +161,16 @@ __global__ __launch_bounds__(256) void gate_linear_kernel(LinArgs p) {
   const int full = p.K / 256;
   const int mine_full = full > part ? (full - part + S - 1) / S : 0;
   constexpr int kUnroll = R == 1 ? 8 : 4;
+  // items start at different chunks (wrapping round), so that the workgroups
+  // of a launch do not all read the same stretch of the shared inputs at the
+  // same time: they would queue on the same L2 channels
+  const int rot = mine_full > 0 ? (int)((((uint32_t)item * 2654435761u) >> 8) % (uint32_t)mine_full) : 0;
 #pragma unroll kUnroll
-  for (int i = 0; i < mine_full; ++i) step((part + i * S) * 256 + 4 * lane);
+  for (int i = 0; i < mine_full; ++i) {
+    int c = i + rot;
+    c = c >= mine_full ? c - mine_full : c;
+    step((part + c * S) * 256 + 4 * lane);
+  }
   if (full % S == part && full * 256 + 4 * lane < p.K) step(full * 256 + 4 * lane);
 
   // reduce over the wavefront; lane j * 8 + bi keeps row j, request bi
