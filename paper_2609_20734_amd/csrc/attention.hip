@@ -40,9 +40,6 @@
 #ifndef ODA_KV_NONTEMPORAL
 #define ODA_KV_NONTEMPORAL 1
 #endif
-#ifndef ODA_SPLIT_PREFETCH
-#define ODA_SPLIT_PREFETCH 0
-#endif
 #ifndef ODA_FUSED_MERGE
 #define ODA_FUSED_MERGE 1   // 0: merge split-K partials in a second launch
 #endif
@@ -578,30 +575,6 @@ void attn_split_kernel(AttnArgs a) {
     int bad = 0;
     int tbl = table_chunk(r, 0, lane, bad);
     int tbl_next = table_chunk(r, 1, lane, bad);
-#if ODA_SPLIT_PREFETCH
-    PairTile<D> ta, tb;
-    load_pair<D>(ta, r, r.v_lo, tbl, lane);
-    for (int v = r.v_lo; v < r.v_hi; v += 4) {
-      const bool more1 = v + 2 < r.v_hi;
-      if (more1) {
-        if (((v + 2 - r.v_lo) & 63) == 0) {   // entering the next 64-block chunk of the table
-          tbl = tbl_next;
-          tbl_next = table_chunk(r, ((v + 2 - r.v_lo) >> 6) + 1, lane, bad);
-        }
-        load_pair<D>(tb, r, v + 2, tbl, lane);
-      }
-      consume_pair<D>(ta, r, v, lane, qf, a.scale_log2, o, m_run, l_run);
-      if (!more1) break;
-      if (v + 4 < r.v_hi) {
-        if (((v + 4 - r.v_lo) & 63) == 0) {
-          tbl = tbl_next;
-          tbl_next = table_chunk(r, ((v + 4 - r.v_lo) >> 6) + 1, lane, bad);
-        }
-        load_pair<D>(ta, r, v + 4, tbl, lane);
-      }
-      consume_pair<D>(tb, r, v + 2, lane, qf, a.scale_log2, o, m_run, l_run);
-    }
-#else
     for (int v = r.v_lo; v < r.v_hi; v += 2) {
       if (v > r.v_lo && ((v - r.v_lo) & 63) == 0) {
         tbl = tbl_next;
@@ -611,7 +584,6 @@ void attn_split_kernel(AttnArgs a) {
       load_pair<D>(ta, r, v, tbl, lane);
       consume_pair<D>(ta, r, v, lane, qf, a.scale_log2, o, m_run, l_run);
     }
-#endif
     l_run += __shfl_xor(l_run, 16);
     l_run += __shfl_xor(l_run, 32);
     if (__any(bad)) {   // a block-table entry out of range: this request's rows become NaN
