@@ -60,7 +60,9 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int kBlock = 16;            // positions per KV block
 constexpr int kMaxGroup = 16;         // query heads per KV head held by one MFMA tile
 constexpr int kWaves = ODA_SPLIT_WAVES;   // wavefronts per split workgroup
-constexpr int kMergeThreads = 256;
+#if !ODA_FUSED_MERGE
+constexpr int kMergeThreads = 256;    // threads of the separate merge kernel
+#endif
 constexpr int kMergeChunk = 16;       // split partials read per round trip in the merge
 constexpr int kMergeSmall = 4;        // chunk used for the last few splits
 constexpr float kLog2e = 1.4426950408889634f;
@@ -143,6 +145,7 @@ __device__ __forceinline__ bool block_full(const Geometry& g, int lb) {
   return p1 <= g.a_end || (p0 >= g.r_start && p1 <= g.nc);
 }
 
+#if !ODA_FUSED_MERGE
 // Map a slot of the request dimension to a request id; false if the slot has
 // no selected request.
 __device__ __forceinline__ bool resolve_request(const AttnArgs& a, int slot, int& b) {
@@ -155,6 +158,7 @@ __device__ __forceinline__ bool resolve_request(const AttnArgs& a, int slot, int
   if (a.select == kSelFlags) return a.flags[slot] != 0;
   return true;
 }
+#endif
 
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
@@ -190,7 +194,7 @@ __device__ __forceinline__ bool request_of_rank(const AttnArgs& a, int rank, int
     if (rank < seen + c) {
       // the lane whose flag is set with exactly rank - seen set flags below it
       const uint64_t below = m & ((1ull << lane) - 1ull);
-      const bool hit = ((m >> lane) & 1ull) != 0 && __popcll(below) == rank - seen;
+      const bool hit = ((m >> lane) & 1ull) != 0 && (int)__popcll(below) == rank - seen;
       b = b0 + __builtin_ctzll(__ballot(hit));
       return true;
     }
