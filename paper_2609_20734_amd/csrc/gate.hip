@@ -612,15 +612,16 @@ struct GateWs {
 };
 
 // Workgroups of a split-hidden block (0 if the batch or width does not take
-// that path): 64, or fewer when the hidden width 2 dt has fewer multiples of 4
-// hidden units per workgroup; the partial sums the next launch adds must stay
-// small (<= 256 KiB per consumer workgroup).
+// that path): the most (at most 64) that split the hidden width 2 dt into
+// equal shares of 4, 8 or 16 units, i.e. 1, 2 or 4 per wavefront (the block
+// kernel's instances); the partial sums the next launch adds must stay small
+// (<= 256 KiB per consumer workgroup).
 int split_groups(int64_t B, int64_t dt) {
   if (B > kSplitMaxB || dt > kSplitMaxDt || dt % 4) return 0;
   for (int nw = 64; nw >= 1; nw /= 2) {
     if ((2 * dt) % nw) continue;
     const int64_t hs = 2 * dt / nw;
-    if (hs % kWaves || hs > kSplitMaxHs) continue;
+    if (hs != kWaves && hs != 2 * kWaves && hs != 4 * kWaves) continue;
     if ((int64_t)nw * B * dt * 4 > 256 * 1024) return 0;
     return nw;
   }
@@ -826,16 +827,16 @@ extern "C" oda_status oda_recall_gate(const oda_gate_desc* gate, int32_t batch, 
         sa.B = batch;
         sa.hs = 2 * dt / nw;
         sa.eps = gate->rms_eps;
-        const int hw = sa.hs / kWaves;
+        const int hw = sa.hs / kWaves;   // 1, 2 or 4: split_groups allows no other
         const dim3 g((unsigned)nw), t(256);
         if (dt <= 256) {
           if (hw == 1) hipLaunchKernelGGL((gate_split_block_kernel<1, 1>), g, t, 0, stream, sa);
           else if (hw == 2) hipLaunchKernelGGL((gate_split_block_kernel<2, 1>), g, t, 0, stream, sa);
-          else hipLaunchKernelGGL((gate_split_block_kernel<4, 1>), g, t, 0, stream, sa);
+          else hipLaunchKernelGGL((gate_split_block_kernel<4, 1>), g, t, 0, stream, sa);   // hw == 4
         } else {
           if (hw == 1) hipLaunchKernelGGL((gate_split_block_kernel<1, 2>), g, t, 0, stream, sa);
           else if (hw == 2) hipLaunchKernelGGL((gate_split_block_kernel<2, 2>), g, t, 0, stream, sa);
-          else hipLaunchKernelGGL((gate_split_block_kernel<4, 2>), g, t, 0, stream, sa);
+          else hipLaunchKernelGGL((gate_split_block_kernel<4, 2>), g, t, 0, stream, sa);   // hw == 4
         }
       }
       fa.X = z1;

@@ -31,7 +31,7 @@ def _case(seed):
     return L, B, Hkv * G, Hkv, D, seq, s, w, split, cur, mode, flags
 
 
-@pytest.mark.parametrize("seed", range(24))
+@pytest.mark.parametrize("seed", range(200))
 def test_random_problems(seed):
     L, B, Hq, Hkv, D, seq, s, w, split, cur, mode, flags = _case(seed)
     pb = AttnProblem(2000 + seed, L, B, Hq, Hkv, D, seq, cur=cur, split_blocks=split)

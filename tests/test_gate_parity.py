@@ -70,7 +70,12 @@ def _check(g, h, e, l, tau, forced=None):
                                          ("paper", 2048, 1024, 1), ("paper", 4096, 260, 70),
                                          ("paper", 256, 516, 2), ("mlp", 8192, 512, 8), ("mlp", 4096, 256, 70),
                                          # split-hidden SwiGLU blocks (one or two requests)
-                                         ("paper", 1024, 128, 2), ("paper", 4096, 512, 1), ("paper", 256, 32, 2)])
+                                         ("paper", 1024, 128, 2), ("paper", 4096, 512, 1), ("paper", 256, 32, 2),
+                                         # tower widths whose hidden units do not split into 1, 2 or 4 per
+                                         # wavefront: unsplit blocks (these once ran the split kernel of
+                                         # another width)
+                                         ("paper", 1732, 192, 1), ("paper", 512, 384, 2), ("paper", 300, 96, 1),
+                                         ("paper", 64, 12, 2)])
 def test_scores_and_flags(kind, d, dh, B):
     g = Gate(kind, d, dh, B)
     h, e, l = (x[0] for x in S.gate_inputs(3, 1, B, d))
