@@ -62,10 +62,11 @@ def dense(w_bits, x, gain=None, eps: float = 1e-6, residual=None):
 
 
 def swiglu(w_bits, x, gain, eps: float):
-    """SiLU(W_g . x') * (W_u . x'); w_bits holds the gate rows, then the up rows."""
+    """SiLU(W_g . x') * (W_u . x'); w_bits holds the gate rows, then the up
+    rows; x' = RMSNorm(x) with `gain`, or x itself (as in `dense`)."""
     W = A.bf16_to_f64(w_bits)
     F = W.shape[0] // 2
-    xin = rmsnorm(x, gain, eps)
+    xin = rmsnorm(x, gain, eps) if gain is not None else np.asarray(x, dtype=np.float64)
     return silu(xin @ W[:F].T) * (xin @ W[F:].T)
 
 

@@ -238,25 +238,26 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(RopeArgs p) {
   const int b = selected_request(p.work_list, slot);
   if (b < 0 || b >= p.B) return;   // a listed request outside the batch is skipped
   const int half = p.D / 2;
-  if (lane >= half) return;
+  const bool active = lane < half;   // lane i holds the pair (i, i + D/2)
   const float* src = p.qkv + ((int64_t)b * heads + h) * p.D;
-  float x1 = src[lane], x2 = src[lane + half];
+  float x1 = active ? src[lane] : 0.f, x2 = active ? src[lane + half] : 0.f;
   uint16_t* dst;
   if (h < p.Hq + p.Hkv) {
     const bool is_q = h < p.Hq;
     const float* gain = is_q ? p.q_gain : p.k_gain;
     if (gain != nullptr) {
-      // a sum over the D/2 active lanes (the others add nothing)
+      // every lane takes part in the sum (the inactive ones add zeros), so it
+      // is whole for any D / 2 up to 64, not only powers of two
       float ss = x1 * x1 + x2 * x2;
 #pragma unroll
-      for (int s = 32; s >= 1; s >>= 1) {
-        const float o = __shfl_xor(ss, s);
-        if ((lane ^ s) < half) ss += o;
-      }
+      for (int s = 32; s >= 1; s >>= 1) ss += __shfl_xor(ss, s);
       const float inv = rsqrtf(ss / (float)p.D + p.eps);
-      x1 = x1 * inv * gain[lane];
-      x2 = x2 * inv * gain[lane + half];
+      if (active) {
+        x1 = x1 * inv * gain[lane];
+        x2 = x2 * inv * gain[lane + half];
+      }
     }
+    if (!active) return;
     const double pos = (double)(p.seq_lens[b] - 1);
     const double ang = pos * pow(p.theta, -(double)(2 * lane) / (double)p.D);
     const float c = (float)cos(ang), s = (float)sin(ang);
@@ -266,6 +267,7 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(RopeArgs p) {
     x2 = r2;
     dst = is_q ? p.q_out + ((int64_t)b * p.Hq + h) * p.D : p.k_out + ((int64_t)b * p.Hkv + (h - p.Hq)) * p.D;
   } else {
+    if (!active) return;
     dst = p.v_out + ((int64_t)b * p.Hkv + (h - p.Hq - p.Hkv)) * p.D;
   }
   dst[lane] = to_bf16(x1);

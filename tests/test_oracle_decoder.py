@@ -59,6 +59,11 @@ def test_dense_and_swiglu_match_torch():
     y = torch.nn.functional.linear(xn, Wt)
     want = torch.nn.functional.silu(y[:, :5]) * y[:, 5:]
     np.testing.assert_allclose(OD.swiglu(W, x, gain, 1e-5), want.numpy(), rtol=1e-12, atol=1e-12)
+    # no gain: no normalisation, for both modes (the dense ABI's NULL norm gain)
+    y0 = torch.nn.functional.linear(xt, Wt)
+    np.testing.assert_allclose(OD.dense(W, x), y0.numpy(), rtol=1e-12, atol=1e-12)
+    want0 = torch.nn.functional.silu(y0[:, :5]) * y0[:, 5:]
+    np.testing.assert_allclose(OD.swiglu(W, x, None, 1e-5), want0.numpy(), rtol=1e-12, atol=1e-12)
 
 
 def _worked_model():
