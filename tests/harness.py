@@ -61,12 +61,13 @@ class AttnProblem:
     copies for the kernels (identical bits)."""
 
     def __init__(self, seed, L, B, Hq, Hkv, D, seq, permute=True, cur=False, split_blocks=0,
-                 extra_blocks=5, max_blocks_per_seq=None):
+                 extra_blocks=5, max_blocks_per_seq=None, max_len=None):
         self.P = need_gpu()
         self.L, self.B, self.Hq, self.Hkv, self.D = L, B, Hq, Hkv, D
         self.seq = np.asarray(seq, dtype=np.int32)
         self.q = S.normal_bf16(S.rng(seed, S.STREAM_Q), (L, B, Hq, D))
-        mb = max_blocks_per_seq or max(1, int(math.ceil(self.seq.max() / 16)))
+        max_len = max_len or int(self.seq.max())
+        mb = max_blocks_per_seq or max(1, int(math.ceil(max_len / 16)))
         self.table, self.nb = S.paged_block_table(S.rng(seed, S.STREAM_TABLE), self.seq, mb, permute=permute,
                                                   extra_blocks=extra_blocks)
         self.k, self.v = S.kv_cache(seed, L, self.nb, Hkv, D)
@@ -75,7 +76,7 @@ class AttnProblem:
             self.kc = S.normal_bf16(S.rng(seed, S.STREAM_KCUR), (L, B, Hkv, D))
             self.vc = S.normal_bf16(S.rng(seed, S.STREAM_VCUR), (L, B, Hkv, D))
         self.scale = 1.0 / math.sqrt(D)
-        self.shape = self.P.Shape(L, B, Hq, Hkv, D, mb, int(self.seq.max()), self.nb, split_blocks)
+        self.shape = self.P.Shape(L, B, Hq, Hkv, D, mb, max_len, self.nb, split_blocks)
         self.upload()
 
     def upload(self):

@@ -1,6 +1,7 @@
 """Seeded random decode-attention problems against the fp64 oracle: layer
 counts, batch, GQA group, head dimension, lengths, sinks, windows, split
-sizes, candidate K/V and the Full selection mode all drawn per case.  One
+sizes, candidate K/V, the Full selection mode, a native window for Full and
+a length bound above the longest request all drawn per case.  One
 zero-filled workspace serves every call of a case (Local, then Full over the
 flags or the compacted list), so the in-launch split merge and its ticket
 words are exercised across calls with different plans."""
@@ -19,7 +20,7 @@ def _case(seed):
     L = int(g.integers(1, 4))
     B = int(g.integers(1, 6))
     Hkv = int(g.choice([1, 2, 4]))
-    G = int(g.choice([1, 2, 4, 8]))
+    G = int(g.choice([1, 2, 4, 8, 16]))
     D = int(g.choice([64, 128]))
     seq = g.integers(1, 601, size=B).tolist()
     s = int(g.integers(0, 21))
@@ -28,15 +29,17 @@ def _case(seed):
     cur = bool(g.integers(0, 2))
     mode = str(g.choice(["flags", "list", "all"]))
     flags = (g.random(B) < 0.5).astype(np.int32)
-    return L, B, Hkv * G, Hkv, D, seq, s, w, split, cur, mode, flags
+    native = int(g.choice([0, 0, int(g.integers(1, 701))]))     # Full: whole history or a native window
+    slack = int(g.choice([0, 0, int(g.integers(1, 200))]))      # max_seq_len above the longest request
+    return L, B, Hkv * G, Hkv, D, seq, s, w, split, cur, mode, flags, native, slack
 
 
 @pytest.mark.parametrize("seed", range(200))
 def test_random_problems(seed):
-    L, B, Hq, Hkv, D, seq, s, w, split, cur, mode, flags = _case(seed)
-    pb = AttnProblem(2000 + seed, L, B, Hq, Hkv, D, seq, cur=cur, split_blocks=split)
+    L, B, Hq, Hkv, D, seq, s, w, split, cur, mode, flags, native, slack = _case(seed)
+    pb = AttnProblem(2000 + seed, L, B, Hq, Hkv, D, seq, cur=cur, split_blocks=split, max_len=max(seq) + slack)
     P = pb.P
-    ws = torch.zeros(max(256, P.attn_workspace_size(pb.shape, s, w), P.attn_workspace_size(pb.shape, 0, 0)),
+    ws = torch.zeros(max(256, P.attn_workspace_size(pb.shape, s, w), P.attn_workspace_size(pb.shape, 0, native)),
                      dtype=torch.uint8, device="cuda")
     out, lse = pb.new_out(np.nan)
     P.local_decode_attn(pb.shape, pb.inp, s, w, out, lse, ws)
@@ -49,9 +52,9 @@ def test_random_problems(seed):
     fl = dev_i32(flags) if mode == "flags" else None
     wl = dev_i32(sel + [0] * (B - len(sel))) if mode == "list" else None
     nw = dev_i32([len(sel)]) if mode == "list" else None
-    P.full_decode_attn(pb.shape, pb.inp, 0, fl, wl, nw, out, lse, ws)
+    P.full_decode_attn(pb.shape, pb.inp, native, fl, wl, nw, out, lse, ws)
     torch.cuda.synchronize()
-    full, full_lse, _ = pb.oracle_full()
+    full, full_lse, _ = pb.oracle_full(native)
     o, ls = out.cpu().numpy(), lse.cpu().numpy()
     for b in range(B):
         ref, ref_lse = (full, full_lse) if b in sel else (want, want_lse)
