@@ -93,6 +93,7 @@ struct AttnArgs {
   int32_t bps, max_splits;  // bps: blocks per split when fixed by the caller
   int32_t dyn_splits;       // 1: blocks per split chosen on the device (effective_bps)
   int32_t nvb_max;          // host bound on visited blocks per request
+  int32_t lpi;              // layers per work item (attn_local_layers_kernel)
   int32_t select;
   float scale_log2;         // scale * log2(e)
   // device-data checks: a length outside [1, max_len], a block-table entry
@@ -499,63 +500,20 @@ __device__ __forceinline__ void merge_unit(const AttnArgs& a, int l, int b, int 
   }
 }
 
-// kLocal selects the Local access set (sinks + window); Full instances take the
-// native set (whole history, or a native window) and never have sinks.
+// One unit of work: the wavefront runs of r (this split of request b) for
+// layer l and KV head g are streamed, combined across the wavefronts in
+// shared memory and written out (finalised when the request has one split,
+// else as this split's partial).
 template <int D, bool kLocal>
-__global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
-void attn_split_kernel(AttnArgs a) {
+__device__ __forceinline__ void run_unit(const AttnArgs& a, Run& r, int l, int b, int g, int split, int nsplit,
+                                         float* smem) {
   constexpr int KK = D / 32;   // MFMA k-steps for q.k
   constexpr int NT = D / 16;   // 16-dim output tiles
-  extern __shared__ float smem[];
   const int lane = threadIdx.x & 63;
   const int wave = uniform(threadIdx.x >> 6);
   const int h16 = lane & 15;
   const int j = lane >> 4;
-
-  // split outermost, then the rank of the request among those with work: the
-  // items that have work (the splits in use of the selected requests) form a
-  // prefix of the grid, so the dispatcher spreads them over the CUs first
-  // instead of interleaving them with workgroups that exit at once
-  const int active = active_requests(a);
-  if (active == 0) return;
-  int64_t item = blockIdx.x;
-  const int g = (int)(item % a.Hkv);
-  item /= a.Hkv;
-  const int l = (int)(item % a.L);
-  item /= a.L;
-  const int rank = (int)(item % active);
-  if (item / active >= a.max_splits) return;
-  const int split = (int)(item / active);
-  int b;
-  if (!request_of_rank(a, rank, b)) return;
-  b = uniform(b);
-  const int n = uniform(a.seq_lens[b]);
   const int G = a.G;
-  if (!valid_len(a, n)) {   // no history is addressed: the request's rows become NaN
-    if (split == 0) {
-      const int64_t q0 = (((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G) * D;
-      for (int e = threadIdx.x; e < G * D; e += kWaves * 64) {
-        a.out[q0 + e] = __builtin_nanf("");
-        if (e % D == 0 && a.lse != nullptr) a.lse[((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G + e / D] = __builtin_nanf("");
-      }
-    }
-    return;
-  }
-  Run r;
-  r.geo = geometry(n, kLocal ? a.n_sink : 0, a.window, a.has_cur);
-  const int bps = effective_bps(a, active);
-  // (nvb = 0 happens only with the candidate as the sole position: one item, no blocks)
-  const int nsplit = max(1, (r.geo.nvb + bps - 1) / bps);
-  if (split >= nsplit) return;   // uniform over the workgroup: no barrier is skipped by part of it
-
-  // this wavefront's run: a contiguous share of the split's pairs
-  const int v_begin = split * bps;
-  const int v_end = min(r.geo.nvb, v_begin + bps);
-  const int pairs = (v_end - v_begin + 1) >> 1;
-  const int per_wave = (pairs + kWaves - 1) / kWaves;
-  r.v_lo = min(v_end, v_begin + 2 * per_wave * wave);
-  r.v_hi = min(v_end, r.v_lo + 2 * per_wave);
-
   const int64_t head_elems = (int64_t)kBlock * D;
   r.kbase = a.k_cache + (int64_t)l * a.kv_layer_stride + (int64_t)g * head_elems;
   r.vbase = a.v_cache + (int64_t)l * a.kv_layer_stride + (int64_t)g * head_elems;
@@ -667,6 +625,68 @@ void attn_split_kernel(AttnArgs a) {
       }
     }
   }
+}
+
+// kLocal selects the Local access set (sinks + window); Full instances take the
+// native set (whole history, or a native window) and never have sinks.
+template <int D, bool kLocal>
+__global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
+void attn_split_kernel(AttnArgs a) {
+  constexpr int KK = D / 32;   // MFMA k-steps for q.k
+  constexpr int NT = D / 16;   // 16-dim output tiles
+  extern __shared__ float smem[];
+  const int lane = threadIdx.x & 63;
+  const int wave = uniform(threadIdx.x >> 6);
+  const int h16 = lane & 15;
+  const int j = lane >> 4;
+
+  // split outermost, then the rank of the request among those with work: the
+  // items that have work (the splits in use of the selected requests) form a
+  // prefix of the grid, so the dispatcher spreads them over the CUs first
+  // instead of interleaving them with workgroups that exit at once
+  const int active = active_requests(a);
+  if (active == 0) return;
+  int64_t item = blockIdx.x;
+  const int g = (int)(item % a.Hkv);
+  item /= a.Hkv;
+  const int l = (int)(item % a.L);
+  item /= a.L;
+  const int rank = (int)(item % active);
+  if (item / active >= a.max_splits) return;
+  const int split = (int)(item / active);
+  int b;
+  if (!request_of_rank(a, rank, b)) return;
+  b = uniform(b);
+  const int n = uniform(a.seq_lens[b]);
+  const int G = a.G;
+  if (!valid_len(a, n)) {   // no history is addressed: the request's rows become NaN
+    if (split == 0) {
+      const int64_t q0 = (((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G) * D;
+      for (int e = threadIdx.x; e < G * D; e += kWaves * 64) {
+        a.out[q0 + e] = __builtin_nanf("");
+        if (e % D == 0 && a.lse != nullptr) a.lse[((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G + e / D] = __builtin_nanf("");
+      }
+    }
+    return;
+  }
+  Run r;
+  r.geo = geometry(n, kLocal ? a.n_sink : 0, a.window, a.has_cur);
+  const int bps = effective_bps(a, active);
+  // (nvb = 0 happens only with the candidate as the sole position: one item, no blocks)
+  const int nsplit = max(1, (r.geo.nvb + bps - 1) / bps);
+  if (split >= nsplit) return;   // uniform over the workgroup: no barrier is skipped by part of it
+
+  // this wavefront's run: a contiguous share of the split's pairs
+  const int v_begin = split * bps;
+  const int v_end = min(r.geo.nvb, v_begin + bps);
+  const int pairs = (v_end - v_begin + 1) >> 1;
+  const int per_wave = (pairs + kWaves - 1) / kWaves;
+  r.v_lo = min(v_end, v_begin + 2 * per_wave * wave);
+  r.v_hi = min(v_end, r.v_lo + 2 * per_wave);
+
+  run_unit<D, kLocal>(a, r, l, b, g, split, nsplit, smem);
+  const bool finalize = (nsplit == 1);
+  float* sm_zc = smem + kWaves * 32 + kWaves * G * D;
 #if ODA_FUSED_MERGE
   if (finalize) return;
   // The last of the request's splits to finish merges them all.  The eight
@@ -691,6 +711,50 @@ void attn_split_kernel(AttnArgs a) {
   merge_unit<D>(a, l, b, g, nsplit, sm_zc, kWaves * 64);
   if (threadIdx.x == 0) __hip_atomic_store(ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #endif
+}
+
+// Batched Local with one split per unit and many units per CU: a work item is
+// a.lpi consecutive layers of one (request, KV head), walked in turn by the
+// workgroup.  The request's length is read once for all of them and each
+// layer starts on a CU that is already running (no workgroup start-up per
+// unit).  Items: (KV head, layer group, request), KV head fastest.
+template <int D>
+__global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
+void attn_local_layers_kernel(AttnArgs a) {
+  extern __shared__ float smem[];
+  const int wave = uniform(threadIdx.x >> 6);
+  int64_t item = blockIdx.x;
+  const int g = (int)(item % a.Hkv);
+  item /= a.Hkv;
+  const int groups = a.L / a.lpi;
+  const int lg = (int)(item % groups);
+  item /= groups;
+  if (item >= a.B) return;
+  const int b = (int)item;
+  const int n = uniform(a.seq_lens[b]);
+  const int G = a.G;
+  const int l0 = lg * a.lpi, l1 = l0 + a.lpi;
+  if (!valid_len(a, n)) {   // no history is addressed: the request's rows become NaN
+    for (int l = l0; l < l1; ++l) {
+      const int64_t q0 = (((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G) * D;
+      for (int e = threadIdx.x; e < G * D; e += kWaves * 64) {
+        a.out[q0 + e] = __builtin_nanf("");
+        if (e % D == 0 && a.lse != nullptr) a.lse[((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G + e / D] = __builtin_nanf("");
+      }
+    }
+    return;
+  }
+  Run r;
+  r.geo = geometry(n, a.n_sink, a.window, a.has_cur);
+  // one split: this wavefront's contiguous share of the unit's pairs
+  const int pairs = (r.geo.nvb + 1) >> 1;
+  const int per_wave = (pairs + kWaves - 1) / kWaves;
+  r.v_lo = min(r.geo.nvb, 2 * per_wave * wave);
+  r.v_hi = min(r.geo.nvb, r.v_lo + 2 * per_wave);
+  for (int l = l0; l < l1; ++l) {
+    run_unit<D, true>(a, r, l, b, g, 0, 1, smem);
+    __syncthreads();   // the next layer reuses the shared memory
+  }
 }
 
 #if !ODA_FUSED_MERGE
@@ -817,8 +881,38 @@ oda_status check_inputs(const oda_attn_inputs* in, const float* out) {
   return ODA_OK;
 }
 
+// Layers per work item of a Local call: the most (a divisor of L) that still
+// leave at least ODA_TARGET_GROUPS workgroups, when every unit has one split;
+// 1 (the split kernel) otherwise.
+int layers_per_item(const oda_attn_shape* s, const Plan& plan) {
+  if (plan.max_splits != 1) return 1;
+  const int64_t per_layer = (int64_t)s->batch * s->num_kv_heads;
+  for (int d = s->num_layers; d > 1; --d)
+    if (s->num_layers % d == 0 && (s->num_layers / d) * per_layer >= ODA_TARGET_GROUPS) return d;
+  return 1;
+}
+
+template <int D>
+oda_status launch_layers(const AttnArgs& args, hipStream_t stream) {
+  const int64_t items = (int64_t)(args.L / args.lpi) * args.B * args.Hkv;
+  if (items > 0x7fffffffLL) return oda::fail(ODA_ERR_SHAPE, "grid too large (%lld work items)", (long long)items);
+  const size_t lds = split_lds_floats(args.G, D) * sizeof(float);
+  static bool lds_raised = false;
+  if (!lds_raised) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(attn_local_layers_kernel<D>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)(split_lds_floats(kMaxGroup, D) * 4));
+    lds_raised = true;
+  }
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(attn_local_layers_kernel<D>, dim3((unsigned)items), dim3(kWaves * 64), lds, stream, args);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return oda::fail(ODA_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ODA_OK;
+}
+
 template <int D, bool kLocal>
 oda_status launch(const AttnArgs& args, const Plan& plan, hipStream_t stream) {
+  if (kLocal && args.lpi > 1) return launch_layers<D>(args, stream);
   const int64_t units = (int64_t)args.L * args.B * args.Hkv;
   const int64_t items = units * plan.max_splits;
   if (items > 0x7fffffffLL) return oda::fail(ODA_ERR_SHAPE, "grid too large (%lld work items)", (long long)items);
@@ -883,6 +977,7 @@ oda_status run_attention(const oda_attn_shape* s, const oda_attn_inputs* in, boo
   a.max_splits = plan.max_splits;
   a.dyn_splits = plan.dyn;
   a.nvb_max = plan.nvb_max;
+  a.lpi = local ? layers_per_item(s, plan) : 1;
   a.select = select;
   a.scale_log2 = in->scale * kLog2e;
   oda_status st;

@@ -126,6 +126,31 @@ def test_few_selected_of_a_wide_batch(mode):
             assert np.all(o[:, b] == -7.0) and np.all(ls[:, b] == -7.0)
 
 
+@pytest.mark.parametrize("L,B,Hkv,cur", [(4, 64, 8, False), (6, 16, 8, True), (8, 32, 8, False), (3, 40, 8, True)])
+def test_local_layer_groups(L, B, Hkv, cur):
+    """Batched Local with enough units that one work item walks several
+    layers of a (request, KV head) in turn (4, 3, 8 and 3 layers here): every
+    layer's rows against the oracle, including a request whose length is out
+    of range (NaN rows in every layer of its groups)."""
+    g = np.random.default_rng(L * 100 + B)
+    seq = g.integers(1, 300, size=B)
+    seq[3] = 290
+    p = AttnProblem(L * 100 + B, L, B, Hkv, Hkv, 64, seq.tolist(), cur=cur)
+    bad = p.seq.copy()
+    bad[5] = 0                                   # outside [1, max_seq_len]
+    p.dseq = dev_i32(bad)
+    p.inp = p.P.inputs(p.dq, p.dk, p.dv, p.dtable, p.dseq, p.scale, p.dkc, p.dvc)
+    out, lse = p.run_local(4, 96)
+    o, ls = out.cpu().numpy(), lse.cpu().numpy()
+    ref, ref_lse, _ = p.oracle_local(4, 96, requests=[b for b in range(B) if b != 5])
+    for b in range(B):
+        if b == 5:
+            assert np.isnan(o[:, b]).all() and np.isnan(ls[:, b]).all()
+            continue
+        check_close(o[:, b], ref[:, b], what=f"request {b}")
+        assert np.max(np.abs(ls[:, b] - ref_lse[:, b])) <= LSE_ABS
+
+
 def test_empty_work_list_writes_nothing():
     p = AttnProblem(2, 1, 3, 8, 2, 64, [10, 20, 30])
     out, lse = p.new_out(3.5)
