@@ -15,6 +15,9 @@
 //             and the workgroup holding the request's last ticket combines
 //             the partials in split order with stable softmax rescaling (plus
 //             the candidate) and writes out / lse: no second launch.
+//   layers -- batched Local whose units all have one split: one workgroup per
+//             (KV head, group of consecutive layers, request) streams the
+//             group's layers in turn with the same per-unit body.
 // This is the split-phase / combine-phase structure the paper's Local path
 // uses (App. A.5), applied to both branches.
 //
