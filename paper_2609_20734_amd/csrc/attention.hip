@@ -635,13 +635,8 @@ __device__ __forceinline__ void run_unit(const AttnArgs& a, Run& r, int l, int b
 template <int D, bool kLocal>
 __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_split_kernel(AttnArgs a) {
-  constexpr int KK = D / 32;   // MFMA k-steps for q.k
-  constexpr int NT = D / 16;   // 16-dim output tiles
   extern __shared__ float smem[];
-  const int lane = threadIdx.x & 63;
   const int wave = uniform(threadIdx.x >> 6);
-  const int h16 = lane & 15;
-  const int j = lane >> 4;
 
   // split outermost, then the rank of the request among those with work: the
   // items that have work (the splits in use of the selected requests) form a
@@ -688,10 +683,9 @@ void attn_split_kernel(AttnArgs a) {
   r.v_hi = min(v_end, r.v_lo + 2 * per_wave);
 
   run_unit<D, kLocal>(a, r, l, b, g, split, nsplit, smem);
-  const bool finalize = (nsplit == 1);
-  float* sm_zc = smem + kWaves * 32 + kWaves * G * D;
 #if ODA_FUSED_MERGE
-  if (finalize) return;
+  if (nsplit == 1) return;   // finalised
+  float* sm_zc = smem + kWaves * 32 + kWaves * G * D;
   // The last of the request's splits to finish merges them all.  The eight
   // XCDs' L2 caches are not coherent with each other, so the partials are
   // published at device scope: every wavefront waits until its stores have
