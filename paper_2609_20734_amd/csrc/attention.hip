@@ -818,13 +818,15 @@ oda_status check_shape(const oda_attn_shape* s) {
 
 // Work decomposition.  One workgroup per (request, layer, KV head, split).
 // The automatic plan splits a request only as much as needed for the selected
-// requests to give the GPU about ODA_TARGET_GROUPS workgroups (one per CU):
-// the grid and the workspace are sized for the case of a single selected
-// request (max_splits); the kernels pick the actual split count on the device
-// (effective_bps).  A request covered by one split is finalised by its
-// workgroup; otherwise the last of its splits merges them in the same launch.
+// requests to give the GPU about ODA_TARGET_GROUPS workgroups (one per CU).
+// Local selects every request; Full's grid and workspace are sized for the
+// case of a single selected request (max_splits), and the kernels pick the
+// actual split count on the device (effective_bps).  The workspace size a
+// caller queries is the single-request one, which covers both.  A request
+// covered by one split is finalised by its workgroup; otherwise the last of
+// its splits merges them in the same launch.
 // Workspace: the ticket words (one per unit), then the partial o, then (m, l).
-void make_plan(const oda_attn_shape* s, int n_sink, int window, Plan* p) {
+void make_plan(const oda_attn_shape* s, int n_sink, int window, int64_t selected, Plan* p) {
   const int64_t total_blocks = oda::ceil_div(s->max_seq_len, kBlock);
   int64_t nvb = total_blocks;
   if (window > 0) {
@@ -832,11 +834,11 @@ void make_plan(const oda_attn_shape* s, int n_sink, int window, Plan* p) {
     nvb = std::min<int64_t>(total_blocks, sink_blocks + oda::ceil_div(window, kBlock) + 1);
   }
   const int64_t units = (int64_t)s->num_layers * s->batch * s->num_kv_heads;
-  const int64_t units_per_request = (int64_t)s->num_layers * s->num_kv_heads;
+  const int64_t units_selected = (int64_t)s->num_layers * s->num_kv_heads * selected;
   int64_t bps = s->split_blocks;
   p->dyn = 0;
   if (bps == 0) {
-    const int64_t want = oda::ceil_div(ODA_TARGET_GROUPS, units_per_request);
+    const int64_t want = oda::ceil_div(ODA_TARGET_GROUPS, units_selected);
     // at least one block pair per wavefront
     const int64_t max_split = std::max<int64_t>(1, nvb / (2 * kWaves));
     const int64_t nsplit = std::max<int64_t>(1, std::min(want, max_split));
@@ -935,7 +937,8 @@ oda_status run_attention(const oda_attn_shape* s, const oda_attn_inputs* in, boo
                          int select, const int32_t* flags, const int32_t* work_list, const int32_t* n_work,
                          float* out, float* lse, void* ws, size_t ws_bytes, hipStream_t stream) {
   Plan plan;
-  make_plan(s, n_sink, window, &plan);
+  // Local attends every request; Full is sized for the fewest selected (one)
+  make_plan(s, n_sink, window, local ? s->batch : 1, &plan);
   if (plan.bytes > 0) {
     if (ws == nullptr) return oda::fail(ODA_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", plan.bytes);
     if (ws_bytes < plan.bytes)
@@ -995,7 +998,7 @@ extern "C" oda_status oda_attn_workspace_size(const oda_attn_shape* shape, int32
   if (bytes == nullptr) return oda::fail(ODA_ERR_NULL, "bytes is NULL");
   if (n_sink < 0 || window < 0) return oda::fail(ODA_ERR_SHAPE, "n_sink and window must be >= 0");
   Plan plan;
-  make_plan(shape, n_sink, window, &plan);
+  make_plan(shape, n_sink, window, 1, &plan);   // covers Local and Full calls of this shape
   *bytes = plan.bytes;
   return oda::ok();
 }
