@@ -35,6 +35,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 
 #include "oda.h"
@@ -891,17 +892,28 @@ int layers_per_item(const oda_attn_shape* s, const Plan& plan) {
   return 1;
 }
 
+// Raise a kernel's dynamic-LDS limit once per device (the attribute belongs
+// to the device's copy of the kernel).  `done` holds one bit per device id
+// below 64; other ids set it on every call.  Host threads that race here set
+// the same value twice, which is harmless.  A failure is not fatal: the
+// launch that needs the limit then fails and reports it.
+void raise_lds_limit(const void* kernel, std::atomic<uint64_t>* done, int bytes) {
+  int dev = -1;
+  (void)hipGetDevice(&dev);
+  const uint64_t bit = (dev >= 0 && dev < 64) ? (1ull << dev) : 0ull;
+  if (bit != 0 && (done->load(std::memory_order_acquire) & bit) != 0) return;
+  if (hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess)
+    done->fetch_or(bit, std::memory_order_acq_rel);
+}
+
 template <int D>
 oda_status launch_layers(const AttnArgs& args, hipStream_t stream) {
   const int64_t items = (int64_t)(args.L / args.lpi) * args.B * args.Hkv;
   if (items > 0x7fffffffLL) return oda::fail(ODA_ERR_SHAPE, "grid too large (%lld work items)", (long long)items);
   const size_t lds = split_lds_floats(args.G, D) * sizeof(float);
-  static bool lds_raised = false;
-  if (!lds_raised) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(attn_local_layers_kernel<D>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)(split_lds_floats(kMaxGroup, D) * 4));
-    lds_raised = true;
-  }
+  static std::atomic<uint64_t> lds_raised{0};
+  raise_lds_limit(reinterpret_cast<const void*>(attn_local_layers_kernel<D>), &lds_raised,
+                  (int)(split_lds_floats(kMaxGroup, D) * 4));
   (void)hipGetLastError();
   hipLaunchKernelGGL(attn_local_layers_kernel<D>, dim3((unsigned)items), dim3(kWaves * 64), lds, stream, args);
   const hipError_t e = hipGetLastError();
@@ -916,12 +928,9 @@ oda_status launch(const AttnArgs& args, const Plan& plan, hipStream_t stream) {
   const int64_t items = units * plan.max_splits;
   if (items > 0x7fffffffLL) return oda::fail(ODA_ERR_SHAPE, "grid too large (%lld work items)", (long long)items);
   const size_t lds = split_lds_floats(args.G, D) * sizeof(float);
-  static bool lds_raised = false;
-  if (!lds_raised) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(attn_split_kernel<D, kLocal>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)(split_lds_floats(kMaxGroup, D) * 4));
-    lds_raised = true;
-  }
+  static std::atomic<uint64_t> lds_raised{0};
+  raise_lds_limit(reinterpret_cast<const void*>(attn_split_kernel<D, kLocal>), &lds_raised,
+                  (int)(split_lds_floats(kMaxGroup, D) * 4));
   (void)hipGetLastError();
   hipLaunchKernelGGL((attn_split_kernel<D, kLocal>), dim3((unsigned)items), dim3(kWaves * 64), lds, stream, args);
 #if !ODA_FUSED_MERGE
