@@ -673,7 +673,11 @@ void launch_linear_rs(const LinArgs& a, hipStream_t stream) {
 // workgroup when rows are long (K >= 4096), or when there are too few items
 // to occupy the chip (< 1024) and every wavefront still gets whole chunks.
 // With more than two requests per tile, R = 4 (else 2) rows share each input
-// load while that still leaves >= 512 workgroups.
+// load while that still leaves >= 512 workgroups.  With one or two, only the
+// tower layer groups rows (R = 2, down to 256 workgroups): its inputs are
+// d_model long, and re-reading them for every row cost more than the wider
+// items (the d = 8192 head took 56 instead of 63 µs at B = 2); in the other
+// layers grouping at small batches measured slower.
 template <int MODE>
 void launch_linear(const LinArgs& a, hipStream_t stream) {
   const int tiles = (int)oda::ceil_div(a.B, kBatchTile);
@@ -682,7 +686,10 @@ void launch_linear(const LinArgs& a, hipStream_t stream) {
   const int64_t items = (int64_t)a.rows * tiles;
   const bool split = a.K >= 4096 || (a.K >= 1024 && items < 1024);
   auto fits = [&](int r) {
-    return per_tile > 2 && unit % r == 0 && items / r / (split ? 1 : kWaves) >= 512;
+    if (unit % r != 0) return false;
+    const int64_t groups = items / r / (split ? 1 : kWaves);
+    if (MODE == kTower && r == 2 && groups >= 256) return true;
+    return per_tile > 2 && groups >= 512;
   };
   if (split) {
     if (fits(4)) return launch_linear_rs<MODE, 4, kWaves>(a, stream);
