@@ -142,9 +142,16 @@ class Model:
             h[req] = dense(w["w_down"][l], m, residual=h[req])
         return h, kc, vc
 
+    def final_state(self, h):
+        """The final normalised hidden state RMSNorm(h) with the final gain:
+        the head's h^L_t for the Local branch (§2.1) and, for the selected
+        branch, the state the vocabulary projection reads, which is the
+        head's h_{t-1} at the next step (App. A.5)."""
+        return rmsnorm(h, self.w["final_norm"], self.eps)
+
     def logits(self, h):
         """W_vocab . RMSNorm(h) with the vocabulary projection tied to the embedding."""
-        return dense(self.w["embed"], h, self.w["final_norm"], self.eps)
+        return dense(self.w["embed"], self.final_state(h))
 
 
 def argmax(x):
@@ -168,13 +175,19 @@ def oda_step(model: Model, tokens, k_cache, v_cache, block_table, seq_lens, n_si
     the Full forward from the same pre-step history for flagged requests, and
     the selected state (App. A.5): its final hidden state, candidates, logits
     and greedy token.  The cache is not modified (oracle.step.commit does
-    that)."""
+    that).
+
+    h^L_t is the final normalised Local hidden state (§2.1), and h_prev is the
+    final normalised selected state of the previous step (App. A.5: the state
+    the vocabulary projection reads); the result's "h_state" is that state
+    for this step, the next step's h_prev."""
     from . import gate as Gt
     B = len(tokens)
     hL, kL, vL = model.forward(tokens, k_cache, v_cache, block_table, seq_lens,
                                lambda n: A.local_set(n, n_sink, window))
     emb = model.embed(tokens)
-    score = score_fn(h_prev, emb, hL)
+    hL_state = model.final_state(hL)
+    score = score_fn(h_prev, emb, hL_state)
     flags = Gt.decide(score, tau, forced)
     work, n_work = Gt.compact(flags)
     h = hL.copy()
@@ -185,6 +198,8 @@ def oda_step(model: Model, tokens, k_cache, v_cache, block_table, seq_lens, n_si
         h[work] = hF[work]
         kF[:, work] = kF_[:, work]
         vF[:, work] = vF_[:, work]
-    logits = model.logits(h)
-    return dict(h_local=hL, score=score, flags=flags.astype(np.int32), work_list=work, n_work=n_work, h=h,
-                k_local=kL, v_local=vL, k_full=kF, v_full=vF, logits=logits, token=argmax(logits))
+    h_state = model.final_state(h)
+    logits = dense(model.w["embed"], h_state)
+    return dict(h_local=hL, h_local_state=hL_state, score=score, flags=flags.astype(np.int32), work_list=work,
+                n_work=n_work, h=h, h_state=h_state, k_local=kL, v_local=vL, k_full=kF, v_full=vF, logits=logits,
+                token=argmax(logits))

@@ -11,8 +11,7 @@ import os
 from dataclasses import dataclass
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-# ODA_LIBRARY may point at another build of the same library (kernel-variant experiments)
-LIB_PATH = os.environ.get("ODA_LIBRARY") or os.path.join(_PKG, "liboda.so")
+LIB_PATH = os.path.join(_PKG, "liboda.so")
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_20734_amd.build` "
@@ -35,8 +34,8 @@ DENSE_SWIGLU = 1
 
 EXPORTED = ("oda_attn_workspace_size", "oda_local_decode_attn", "oda_full_decode_attn",
             "oda_gate_param_count", "oda_gate_workspace_size", "oda_recall_gate", "oda_commit_kv",
-            "oda_dense_bf16", "oda_qk_norm_rope", "oda_embed_bf16", "oda_copy_rows", "oda_argmax",
-            "oda_stream_read", "oda_status_string", "oda_last_error")
+            "oda_dense_bf16", "oda_qk_norm_rope", "oda_embed_bf16", "oda_copy_rows", "oda_rms_norm_rows",
+            "oda_argmax", "oda_stream_read", "oda_status_string", "oda_last_error")
 
 
 class OdaError(RuntimeError):
@@ -105,6 +104,8 @@ _lib.oda_embed_bf16.argtypes = [_V, ctypes.c_int32, ctypes.c_int32, ctypes.c_int
 _lib.oda_embed_bf16.restype = ctypes.c_int
 _lib.oda_copy_rows.argtypes = [ctypes.c_int32, ctypes.c_int32, _V, _V, _V, _V, _V]
 _lib.oda_copy_rows.restype = ctypes.c_int
+_lib.oda_rms_norm_rows.argtypes = [ctypes.c_int32, ctypes.c_int32, _V, _V, ctypes.c_float, _V, _V, _V, _V]
+_lib.oda_rms_norm_rows.restype = ctypes.c_int
 _lib.oda_argmax.argtypes = [ctypes.c_int32, ctypes.c_int32, _V, _V, _V]
 _lib.oda_argmax.restype = ctypes.c_int
 _lib.oda_stream_read.argtypes = [_V, ctypes.c_size_t, _V, ctypes.c_int32, _V]
@@ -269,6 +270,12 @@ def copy_rows(batch: int, row_len: int, src, dst, work_list=None, n_work=None, s
                               _stream(stream)))
 
 
+def rms_norm_rows(batch: int, row_len: int, x, gain, rms_eps: float, y, work_list=None, n_work=None,
+                  stream=None) -> None:
+    _check(_lib.oda_rms_norm_rows(batch, row_len, _ptr(x), _ptr(gain), float(rms_eps), _ptr(y), _ptr(work_list),
+                                  _ptr(n_work), _stream(stream)))
+
+
 def argmax(batch: int, n: int, x, index, stream=None) -> None:
     _check(_lib.oda_argmax(batch, n, _ptr(x), _ptr(index), _stream(stream)))
 
@@ -359,6 +366,13 @@ def prepare_embed(table, vocab: int, d_model: int, batch: int, tokens, x, stream
 def prepare_copy_rows(batch: int, row_len: int, src, dst, work_list=None, n_work=None, stream=None) -> Call:
     args = (batch, row_len, _ptr(src), _ptr(dst), _ptr(work_list), _ptr(n_work), _stream(stream))
     return Call(_lib.oda_copy_rows, args, (src, dst, work_list, n_work))
+
+
+def prepare_rms_norm_rows(batch: int, row_len: int, x, gain, rms_eps: float, y, work_list=None, n_work=None,
+                          stream=None) -> Call:
+    args = (batch, row_len, _ptr(x), _ptr(gain), float(rms_eps), _ptr(y), _ptr(work_list), _ptr(n_work),
+            _stream(stream))
+    return Call(_lib.oda_rms_norm_rows, args, (x, gain, y, work_list, n_work))
 
 
 def prepare_argmax(batch: int, n: int, x, index, stream=None) -> Call:

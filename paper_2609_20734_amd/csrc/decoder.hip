@@ -10,6 +10,8 @@
 //                     request's current position, bf16 q / K / V candidates
 //   oda_embed_bf16    embedding rows of the step's tokens
 //   oda_copy_rows     rows of the selected requests from one buffer to another
+//   oda_rms_norm_rows RMSNorm (with gain) of the selected requests' rows: the
+//                     final normalised hidden state the recall head reads
 //   oda_argmax        greedy token of each request's logits
 //
 // Every kernel can be restricted to a device-side list of requests (the
@@ -33,9 +35,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kWaves = 4;
 constexpr int kTile = 8;   // most requests per wavefront in a dense layer
 
-#ifndef ODA_DENSE_MIN_WAVES
-#define ODA_DENSE_MIN_WAVES 2048   // grouping rows stops short of fewer wavefronts than this
-#endif
+constexpr int kDenseMinWaves = 2048;   // grouping rows stops short of fewer wavefronts than this
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -311,6 +311,36 @@ __global__ __launch_bounds__(256) void copy_rows_kernel(const float* src, float*
     *reinterpret_cast<float4*>(dst + base + k) = *reinterpret_cast<const float4*>(src + base + k);
 }
 
+// One workgroup per selected request slot: y = x / sqrt(mean(x^2) + eps) * gain.
+// The sum of squares is reduced in a fixed order (lanes, then wavefronts), so
+// the result is the same on every run.
+__global__ __launch_bounds__(256) void rms_norm_rows_kernel(const float* x, const float* gain, float eps, float* y,
+                                                           int row_len, int B, const int32_t* work_list,
+                                                           const int32_t* n_work) {
+  __shared__ float sred[4];
+  const int slot = blockIdx.x;
+  if (slot >= selected_count(n_work, B)) return;
+  const int b = selected_request(work_list, slot);
+  if (b < 0 || b >= B) return;   // a listed request outside the batch is skipped
+  const int64_t base = (int64_t)b * row_len;
+  float ss = 0.f;
+  for (int k = threadIdx.x * 4; k < row_len; k += 256 * 4) {
+    const float4 v = *reinterpret_cast<const float4*>(x + base + k);
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+#pragma unroll
+  for (int s = 32; s >= 1; s >>= 1) ss += __shfl_xor(ss, s);
+  if ((threadIdx.x & 63) == 0) sred[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float inv = rsqrtf((sred[0] + sred[1] + sred[2] + sred[3]) / (float)row_len + eps);
+  for (int k = threadIdx.x * 4; k < row_len; k += 256 * 4) {
+    const float4 v = *reinterpret_cast<const float4*>(x + base + k);
+    const float4 g = *reinterpret_cast<const float4*>(gain + k);
+    *reinterpret_cast<float4*>(y + base + k) = make_float4(v.x * inv * g.x, v.y * inv * g.y, v.z * inv * g.z,
+                                                           v.w * inv * g.w);
+  }
+}
+
 constexpr int kArgThreads = 1024;
 
 // Greedy choice: the first index of the largest non-NaN value (-1 if every
@@ -395,7 +425,7 @@ extern "C" oda_status oda_dense_bf16(const oda_dense_desc* desc, int32_t batch, 
   if (!oda::aligned(desc->weight, 16) || !oda::aligned(x, 16) || (desc->norm_gain && !oda::aligned(desc->norm_gain, 16)))
     return oda::fail(ODA_ERR_SHAPE, "weight, x and norm_gain must be 16-byte aligned");
   // requests per wavefront: one, up to four, or up to eight; then the most
-  // rows per wavefront that still leave >= ODA_DENSE_MIN_WAVES wavefronts
+  // rows per wavefront that still leave >= kDenseMinWaves wavefronts
   const int tile = batch == 1 ? 1 : batch <= 4 ? 4 : kTile;
   const int64_t tiles = oda::ceil_div(batch, tile);
   const int N = desc->out_features;
@@ -403,7 +433,7 @@ extern "C" oda_status oda_dense_bf16(const oda_dense_desc* desc, int32_t batch, 
   const int rmax = swiglu ? (tile == 1 ? 4 : 2) : (tile == 1 ? 8 : tile == 4 ? 4 : 2);
   int rows = 1;
   for (int r = rmax; r > 1; r /= 2)
-    if (N % r == 0 && (int64_t)(N / r) * tiles >= ODA_DENSE_MIN_WAVES) {
+    if (N % r == 0 && (int64_t)(N / r) * tiles >= kDenseMinWaves) {
       rows = r;
       break;
     }
@@ -506,6 +536,23 @@ extern "C" oda_status oda_copy_rows(int32_t batch, int32_t row_len, const float*
   (void)hipGetLastError();
   hipLaunchKernelGGL(copy_rows_kernel, dim3((unsigned)batch), dim3(256), 0, stream, src, dst, row_len, batch,
                      work_list, n_work);
+  return launch_status();
+}
+
+extern "C" oda_status oda_rms_norm_rows(int32_t batch, int32_t row_len, const float* x, const float* gain,
+                                       float rms_eps, float* y, const int32_t* work_list, const int32_t* n_work,
+                                       hipStream_t stream) {
+  if (!x || !gain || !y) return oda::fail(ODA_ERR_NULL, "x, gain and y are required");
+  if ((work_list == nullptr) != (n_work == nullptr))
+    return oda::fail(ODA_ERR_NULL, "work_list and n_work must both be NULL or both be set");
+  if (batch < 1 || row_len < 4 || row_len % 4)
+    return oda::fail(ODA_ERR_SHAPE, "batch >= 1 and row_len a positive multiple of 4 required");
+  if (!(rms_eps >= 0.f) || !std::isfinite(rms_eps)) return oda::fail(ODA_ERR_SHAPE, "rms_eps must be >= 0");
+  if (!oda::aligned(x, 16) || !oda::aligned(gain, 16) || !oda::aligned(y, 16))
+    return oda::fail(ODA_ERR_SHAPE, "x, gain and y must be 16-byte aligned");
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(rms_norm_rows_kernel, dim3((unsigned)batch), dim3(256), 0, stream, x, gain, rms_eps, y, row_len,
+                     batch, work_list, n_work);
   return launch_status();
 }
 

@@ -6,14 +6,16 @@ Per step (Alg. 1 with the commit of App. A.5):
 
   local stage   embed the step's tokens; the Local forward (every layer:
                 QKV, q/k norm + rotary, Local attention with the Local
-                candidate, output projection, SwiGLU MLP); the recall gate on
+                candidate, output projection, SwiGLU MLP); the final RMSNorm
+                of the Local hidden state (h^L_t, §2.1); the recall gate on
                 (h_{t-1}, E(x_t), h^L_t), writing flags and the compacted list
   retry stage   the Full forward from the same pre-step history for the listed
                 requests only, then their final hidden rows replace the Local
                 ones (App. A.5: only the selected state is kept)
-  output stage  final norm + vocabulary projection, greedy token, the fused
-                commit of the selected candidates of every layer, h_{t-1} for
-                the next step
+  output stage  the final RMSNorm of the selected state (this is h_{t-1} of
+                the next step's gate, App. A.5) and the vocabulary projection
+                of it, greedy token, the fused commit of the selected
+                candidates of every layer
 
 Native Full (always Full, no gate) and standalone Local (no gate, no retry)
 use the same pieces.  Stages are lists of pre-marshalled calls, so they can be
@@ -81,7 +83,8 @@ class Decoder:
         self.emb = torch.zeros(B, d, **f32)
         self.h = torch.zeros(B, d, **f32)               # selected state (Local stream, then selected)
         self.h_full = torch.zeros(B, d, **f32)          # Full retry stream
-        self.h_prev = torch.zeros(B, d, **f32)
+        self.h_prev = torch.zeros(B, d, **f32)         # final-normalised selected state of the last step
+        self.h_local = torch.zeros(B, d, **f32)        # final-normalised Local state (the gate's h^L_t)
         self.qkv = torch.zeros(B, s.qkv_dim, **f32)
         self.q = torch.zeros(B, Hq, D, **bf)
         self.attn = torch.zeros(B, Hq * D, **f32)
@@ -116,7 +119,8 @@ class Decoder:
         self.d_gu = [P.dense_desc(d, s.d_ffn, P.DENSE_SWIGLU, w["w_gu"][l], w["mlp_norm"][l], s.rms_eps)
                      for l in range(L)]
         self.d_down = [P.dense_desc(s.d_ffn, d, P.DENSE_PLAIN, w["w_down"][l]) for l in range(L)]
-        self.d_vocab = P.dense_desc(d, s.vocab, P.DENSE_PLAIN, w["embed"], w["final_norm"], s.rms_eps)
+        # the vocabulary projection reads the final-normalised state (h_prev after the output stage's norm)
+        self.d_vocab = P.dense_desc(d, s.vocab, P.DENSE_PLAIN, w["embed"])
 
     # -- stages ---------------------------------------------------------------
     def _forward(self, h, k_cand, v_cand, branch: str, listed: bool):
@@ -148,11 +152,11 @@ class Decoder:
 
     def _output(self, k_full=None, v_full=None, flags=None):
         s, B = self.shape, self.B
-        return [P.prepare_dense(self.d_vocab, B, self.h, None, self.logits),
+        return [P.prepare_rms_norm_rows(B, s.d_model, self.h, self.w["final_norm"], s.rms_eps, self.h_prev),
+                P.prepare_dense(self.d_vocab, B, self.h_prev, None, self.logits),
                 P.prepare_argmax(B, s.vocab, self.logits, self.next_token),
                 P.prepare_commit(self.commit_shape(), self.k_cache, self.v_cache, self.table, self.seq_lens,
-                                 self.k_loc, self.v_loc, k_full, v_full, flags, True),
-                P.prepare_copy_rows(B, s.d_model, self.h, self.h_prev)]
+                                 self.k_loc, self.v_loc, k_full, v_full, flags, True)]
 
     def commit_shape(self) -> P.Shape:
         a = self.attn_shape
@@ -164,7 +168,8 @@ class Decoder:
         s, B = self.shape, self.B
         assert self.gate is not None
         local = self._input() + self._forward(self.h, self.k_loc, self.v_loc, "local", False)
-        local.append(P.prepare_gate(self.gate, B, self.h_prev, self.emb, self.h, self.tau, self.forced,
+        local.append(P.prepare_rms_norm_rows(B, s.d_model, self.h, self.w["final_norm"], s.rms_eps, self.h_local))
+        local.append(P.prepare_gate(self.gate, B, self.h_prev, self.emb, self.h_local, self.tau, self.forced,
                                     self.score, self.flags, self.work, self.n_work, self.counter, self.ws_gate))
         retry = [P.prepare_copy_rows(B, s.d_model, self.emb, self.h_full, self.work, self.n_work)]
         retry += self._forward(self.h_full, self.k_full, self.v_full, "full", True)

@@ -195,6 +195,13 @@ def test_decoder_entry_points_reject_bad_arguments(L):
     assert status_of(lambda: L.embed_bf16(None, 100, 64, 2, 0x50000, x, stream=0)) == -1
     assert status_of(lambda: L.copy_rows(2, 6, x, y, stream=0)) == -2
     assert status_of(lambda: L.copy_rows(2, 8, x, y, 0x40000, None, stream=0)) == -1
+    g = 0x80000
+    assert status_of(lambda: L.rms_norm_rows(2, 8, None, g, 1e-6, y, stream=0)) == -1
+    assert status_of(lambda: L.rms_norm_rows(2, 8, x, None, 1e-6, y, stream=0)) == -1
+    assert status_of(lambda: L.rms_norm_rows(2, 6, x, g, 1e-6, y, stream=0)) == -2
+    assert status_of(lambda: L.rms_norm_rows(2, 8, x, g, -1.0, y, stream=0)) == -2
+    assert status_of(lambda: L.rms_norm_rows(2, 8, x + 4, g, 1e-6, y, stream=0)) == -2
+    assert status_of(lambda: L.rms_norm_rows(2, 8, x, g, 1e-6, y, 0x40000, None, stream=0)) == -1
     assert status_of(lambda: L.argmax(2, 10, x, y, stream=0)) == -2
     assert status_of(lambda: L.argmax(0, 8, x, y, stream=0)) == -2
 

@@ -209,6 +209,9 @@ def test_decoder_steps_match_oracle():
         assert int(dec.n_work.item()) == int(forced[step].sum())
         assert _rel_l2(dec.score.cpu().numpy(), r["score"]) <= STEP_REL_L2
         assert _rel_l2(dec.h.cpu().numpy(), r["h"]) <= STEP_REL_L2, f"step {step}: hidden"
+        # the head's inputs: final-normalised Local state and the carried selected state
+        assert _rel_l2(dec.h_local.cpu().numpy(), r["h_local_state"]) <= STEP_REL_L2, f"step {step}: h^L_t"
+        assert _rel_l2(dec.h_prev.cpu().numpy(), r["h_state"]) <= STEP_REL_L2, f"step {step}: h_t"
         assert _rel_l2(dec.logits.cpu().numpy(), r["logits"]) <= STEP_REL_L2, f"step {step}: logits"
         tok = dec.next_token.cpu().numpy()
         for b in range(t.B):
@@ -219,7 +222,7 @@ def test_decoder_steps_match_oracle():
             got = getattr(dec, "k_loc" if name == "k_local" else "v_loc").cpu().view(torch.int16).numpy()
             _bf16_close(got.view(np.uint16), r[name], f"step {step} {name}")
         OS.commit(hk, hv, t.table, hseq, r["k_local"], r["v_local"], r["k_full"], r["v_full"], forced[step])
-        h_prev = r["h"]
+        h_prev = r["h_state"]
         np.testing.assert_array_equal(t.dseq.cpu().numpy(), hseq)
     _bf16_close(t.dk.cpu().numpy().view(np.uint16), hk, "K cache")
     _bf16_close(t.dv.cpu().numpy().view(np.uint16), hv, "V cache")

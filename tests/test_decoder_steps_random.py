@@ -97,6 +97,8 @@ def test_random_decoder_steps(seed):
         np.testing.assert_array_equal(dec.flags.cpu().numpy(), forced[step])
         assert _rel_l2(dec.score.cpu().numpy(), r["score"]) <= STEP_REL_L2
         assert _rel_l2(dec.h.cpu().numpy(), r["h"]) <= STEP_REL_L2, f"step {step}: hidden"
+        assert _rel_l2(dec.h_local.cpu().numpy(), r["h_local_state"]) <= STEP_REL_L2, f"step {step}: h^L_t"
+        assert _rel_l2(dec.h_prev.cpu().numpy(), r["h_state"]) <= STEP_REL_L2, f"step {step}: h_t"
         assert _rel_l2(dec.logits.cpu().numpy(), r["logits"]) <= STEP_REL_L2, f"step {step}: logits"
         tok = dec.next_token.cpu().numpy()
         for b in range(B):
@@ -104,7 +106,7 @@ def test_random_decoder_steps(seed):
             if top[1] - top[0] > 1e-3 * max(1.0, abs(top[1])):
                 assert tok[b] == r["token"][b], (step, b)
         OS.commit(hk, hv, table, hseq, r["k_local"], r["v_local"], r["k_full"], r["v_full"], forced[step])
-        h_prev = r["h"]
+        h_prev = r["h_state"]
         np.testing.assert_array_equal(dseq.cpu().numpy(), hseq)
     _caches_close(dk.cpu().numpy().view(np.uint16), dv.cpu().numpy().view(np.uint16), hk, hv, table, seq0, T, L,
                   Hkv)

@@ -151,6 +151,44 @@ def test_oda_step_selects_the_branch(flags):
     np.testing.assert_array_equal(r["logits"], m.logits(r["h"]))
 
 
+def test_final_state_hand_worked():
+    """RMSNorm with the final gain on a hand-worked row: h = (3, 4), gain
+    (2, 0.5), eps = 0 -> mean(h^2) = 12.5, so the state is (6, 2) / sqrt(12.5)."""
+    w = {"w_qkv": np.zeros((1, 1, 2), np.uint16), "embed": np.zeros((4, 2), np.uint16),
+         "final_norm": np.array([2.0, 0.5], np.float32)}
+    m = OD.Model(w, 1, 1, 2, eps=0.0)
+    np.testing.assert_allclose(m.final_state(np.array([[3.0, 4.0]])), [[1.6970562748477140, 0.5656854249492380]],
+                               rtol=1e-15)
+
+
+def test_oda_step_feeds_the_head_final_normalised_states():
+    """§2.1: the head's Local input is the final normalised Local hidden state;
+    App. A.5: the state the step hands on (the next h_{t-1}) is the final
+    normalised selected state, the one the vocabulary projection reads.  The
+    score function sees exactly (h_prev as given, E(x_t), RMSNorm(h^L))."""
+    m, k, v, table, seq = _small()
+    toks = np.array([5, 6, 7])
+    seen = {}
+
+    def score(hp, e, hl):
+        seen.update(hp=hp.copy(), e=e.copy(), hl=hl.copy())
+        return np.array([1.0, -1.0, 1.0])
+
+    hp = np.arange(3 * 128, dtype=np.float64).reshape(3, 128) / 100.0
+    r = OD.oda_step(m, toks, k, v, table, seq, 4, 24, score, hp, 0.0)
+    hl = m.forward(toks, k, v, table, seq, lambda n: A.local_set(n, 4, 24))[0]
+    g = m.w["final_norm"].astype(np.float64)
+    want = hl / np.sqrt(np.mean(hl * hl, axis=-1, keepdims=True) + m.eps) * g
+    np.testing.assert_allclose(seen["hl"], want, rtol=1e-13, atol=0)
+    np.testing.assert_array_equal(seen["hp"], hp)
+    np.testing.assert_array_equal(seen["e"], m.embed(toks))
+    hs = r["h"] / np.sqrt(np.mean(r["h"] ** 2, axis=-1, keepdims=True) + m.eps) * g
+    np.testing.assert_allclose(r["h_state"], hs, rtol=1e-13, atol=0)
+    np.testing.assert_array_equal(r["flags"], [1, 0, 1])
+    # the gain matters: with a non-unit gain the raw and normalised inputs differ
+    assert not np.allclose(seen["hl"], hl)
+
+
 def test_argmax_first_index_and_nan():
     x = np.array([[1.0, 3.0, 3.0, np.nan], [np.nan] * 4, [-np.inf] * 4, [2.0, np.nan, 5.0, 5.0]])
     np.testing.assert_array_equal(OD.argmax(x), [1, -1, 0, 2])
