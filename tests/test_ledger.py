@@ -78,3 +78,41 @@ def test_ideal_ratios_match_independent_ledger(name, rhos, want, gated_only):
         _, _, fall = BN.bytes_for(wl, seq, None, "mlp")
         bench_ratio = (lb + gb + rho * sum(fb)) / sum(fall)
         assert abs(bench_ratio - (local + gate + rho * retry) / full) < 1e-3
+
+
+def test_always_full_bytes_of_the_llama_stack_by_hand():
+    """Bytes_Full of one 32-layer step over 32,768 positions, added up by hand:
+    K + V rows 32 layers x 8 KV heads x 32,768 positions x 512 B = 4,294,967,296;
+    q 32 x 32 heads x 128 x 2 B = 262,144; out + lse 32 x 32 x 129 x 4 B = 528,384;
+    2,048 block-table entries x 4 B = 8,192."""
+    got = OL.always_full_bytes([32768], 0, 32, 32, 8, 128)
+    assert got == 4_294_967_296 + 262_144 + 528_384 + 8_192 == 4_295_766_016
+
+
+def test_step_bytes_by_hand_and_limits():
+    """Bytes(rho) of a small step, by hand: two requests of 40 and 9 positions,
+    one layer, 2 query / 1 KV head of 16 (64 B per position), s = 4, w = 8,
+    the MLP head 8 -> 4 -> 1.
+      Local: request 0 attends 4 + 8 = 12 positions in blocks {0, 2} -> 768 B
+             of K/V + 2 table entries; request 1 (n = 9) attends all 9 -> 576 B
+             + 1 entry; q 2 x 64 B, out + lse 2 x 2 x 17 x 4 B.
+      Gate: (4 x 8 + 4 + 4 + 1) x 4 B weights + 2 x 8 x 4 B inputs + 2 x 12 + 12 B.
+      Full (request 0 flagged): 40 x 64 B + 3 entries + 64 B q + 136 B out."""
+    seq = [40, 9]
+    local = (12 * 64 + 2 * 4) + (9 * 64 + 1 * 4) + 2 * 64 + 2 * 136
+    gate = (4 * 8 + 4 + 4 + 1) * 4 + 2 * 8 * 4 + 2 * 12 + 12
+    full = 40 * 64 + 3 * 4 + 64 + 136
+    got = OL.step_bytes(seq, [1, 0], 4, 8, 0, 1, 2, 1, 16, "mlp", 8, 4)
+    assert got == dict(local=local, gate=gate, full=full, total=local + gate + full)
+    none = OL.step_bytes(seq, [0, 0], 4, 8, 0, 1, 2, 1, 16, "mlp", 8, 4)
+    assert none["full"] == 0 and none["total"] == local + gate
+    # a window that covers every history: Local reads exactly what Full reads
+    cover = OL.step_bytes(seq, [1, 1], 4, 64, 0, 1, 2, 1, 16, "mlp", 8, 4)
+    assert cover["local"] == cover["full"] == OL.always_full_bytes(seq, 0, 1, 2, 1, 16)
+
+
+def test_gate_bytes_of_the_paper_head_at_qwen3_width():
+    """App. A.2's head for d = 2048 has 28,325,889 fp32 parameters."""
+    g = OL.gate_bytes("paper", 1, 2048, 1024)
+    assert g["weights"] == 4 * 28_325_889
+    assert g["inputs"] == 3 * 2048 * 4
