@@ -22,6 +22,28 @@ LSE_ABS = 1e-4
 FLAG_BORDER = 1e-4
 
 
+# Flag decisions whose fp64 score lies within FLAG_BORDER of the threshold are
+# exempt from the bit-exact comparison (the kernel decides in fp32); they are
+# counted here and reported at the end of the session (conftest).
+FLAG_TALLY = {"decisions": 0, "borderline": 0, "mismatched_borderline": 0, "where": {}}
+
+
+def note_flags(where: str, border, mismatch=None) -> int:
+    """Count one comparison's flag decisions: `border` marks the decisions
+    within FLAG_BORDER of the threshold, `mismatch` (optional) those where
+    the kernel and the oracle disagree.  Returns the borderline count."""
+    border = np.asarray(border, dtype=bool)
+    nb = int(border.sum())
+    FLAG_TALLY["decisions"] += int(border.size)
+    FLAG_TALLY["borderline"] += nb
+    if mismatch is not None:
+        FLAG_TALLY["mismatched_borderline"] += int((np.asarray(mismatch, dtype=bool) & border).sum())
+    if nb:
+        FLAG_TALLY["where"][where] = FLAG_TALLY["where"].get(where, 0) + nb
+        print(f"[flags] {where}: {nb} borderline decision(s) of {border.size}", flush=True)
+    return nb
+
+
 def need_gpu():
     if not torch.cuda.is_available():
         raise RuntimeError("this test needs an MI355X")

@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 
 import oda_synth as S
-from harness import FLAG_BORDER, LSE_ABS, check_close
+from harness import FLAG_BORDER, LSE_ABS, check_close, note_flags
 from oracle import attention as OA
 from oracle import gate as OG
 
@@ -90,6 +90,7 @@ def test_decode_step_from_c(tmp_path):
     assert np.max(np.abs(score - score_ref)) <= 1e-4 * scale_
     want = OG.decide(score_ref, tau)
     border = np.abs(score_ref - tau) < FLAG_BORDER
+    note_flags("C driver", border, flags.astype(bool) != want)
     assert not ((flags.astype(bool) != want) & ~border).any()
     assert n_work == int(flags.sum()) and np.array_equal(work[:n_work], np.flatnonzero(flags))
 

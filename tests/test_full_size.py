@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 import torch
 
-from harness import FLAG_BORDER, check_close
+from harness import FLAG_BORDER, check_close, note_flags
 from oracle import attention as OA
 from oracle import gate as OG
 
@@ -55,6 +55,7 @@ def _check_gate(b, tau):
     flags = b.flags.cpu().numpy().astype(bool)
     want = OG.decide(ref, tau)
     border = np.abs(ref - tau) < FLAG_BORDER
+    note_flags(f"full-size {wl.name} {b.head} head tau={tau:.6g}", border, flags != want)
     assert not np.any((flags != want) & ~border)
     n = int(b.n_work.item())
     assert n == int(flags.sum()) and np.array_equal(b.work.cpu().numpy()[:n], np.flatnonzero(flags))

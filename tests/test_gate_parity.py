@@ -6,7 +6,7 @@ import pytest
 import torch
 
 import oda_synth as S
-from harness import FLAG_BORDER, dev_f32, dev_i32, need_gpu
+from harness import FLAG_BORDER, dev_f32, dev_i32, need_gpu, note_flags
 from oracle import gate as OG
 
 pytestmark = pytest.mark.gpu
@@ -55,7 +55,9 @@ def _check(g, h, e, l, tau, forced=None):
     assert np.max(np.abs(sc[fin] - ref[fin]), initial=0.0) <= SCORE_REL * scale
     want = OG.decide(ref, tau, forced)
     border = fin & (np.abs(ref - tau) < FLAG_BORDER) & (forced is None)
-    mism = (fl.astype(bool) != want) & ~border
+    differ = fl.astype(bool) != want
+    note_flags(f"gate {g.kind} d={g.d} dt={g.dh} B={g.B} tau={tau:.6g}", border, differ)
+    mism = differ & ~border
     assert not mism.any(), np.flatnonzero(mism)
     # compaction: ascending flagged ids of the GPU's own flags, and its count
     assert n == int(fl.sum()) and np.array_equal(wl, np.flatnonzero(fl))
