@@ -196,7 +196,9 @@ oda_status oda_recall_gate(const oda_gate_desc *gate, int32_t batch, const float
  * Request selection:
  *   work_list != NULL (with n_work != NULL): exactly the listed requests
  *                       (work_list[0 .. *n_work-1], distinct, as
- *                       oda_recall_gate writes them);
+ *                       oda_recall_gate writes them; a request listed twice
+ *                       gets unspecified rows, but the workspace and every
+ *                       other request are unaffected);
  *   else flags != NULL: the requests with flags[b] != 0;
  *   else              : every request.
  * Only selected requests read KV; only their rows of out (and lse, if not
@@ -292,6 +294,14 @@ oda_status oda_embed_bf16(const uint16_t *table, int32_t vocab, int32_t d_model,
  * selected state. */
 oda_status oda_copy_rows(int32_t batch, int32_t row_len, const float *src, float *dst,
                          const int32_t *work_list, const int32_t *n_work, hipStream_t stream);
+
+/* y[b] = x[b] / sqrt(mean(x[b]^2) + rms_eps) * gain for the listed requests
+ * (all if the list is NULL): the final normalised hidden state, which §2.1
+ * names as the recall head's Local input h_t^L and App. A.5 as the selected
+ * state h_{t-1} the head reads at the next step.  x, y fp32 [batch][row_len]
+ * (row_len a multiple of 4, 16-byte aligned; y may be x), gain fp32 [row_len]. */
+oda_status oda_rms_norm_rows(int32_t batch, int32_t row_len, const float *x, const float *gain, float rms_eps,
+                             float *y, const int32_t *work_list, const int32_t *n_work, hipStream_t stream);
 
 /* index[b] = the first position of the largest non-NaN value of x[b][0..n)
  * (-1 if all are NaN); x fp32 [batch][n], n a multiple of 4. */

@@ -41,19 +41,6 @@
 #include "oda.h"
 #include "oda_internal.h"
 
-#ifndef ODA_KV_NONTEMPORAL
-#define ODA_KV_NONTEMPORAL 1
-#endif
-#ifndef ODA_FUSED_MERGE
-#define ODA_FUSED_MERGE 1   // 0: merge split-K partials in a second launch
-#endif
-#ifndef ODA_SPLIT_WAVES
-#define ODA_SPLIT_WAVES 8
-#endif
-#ifndef ODA_TARGET_GROUPS
-#define ODA_TARGET_GROUPS 256
-#endif
-
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -63,10 +50,8 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kBlock = 16;            // positions per KV block
 constexpr int kMaxGroup = 16;         // query heads per KV head held by one MFMA tile
-constexpr int kWaves = ODA_SPLIT_WAVES;   // wavefronts per split workgroup
-#if !ODA_FUSED_MERGE
-constexpr int kMergeThreads = 256;    // threads of the separate merge kernel
-#endif
+constexpr int kWaves = 8;             // wavefronts per split workgroup
+constexpr int kTargetGroups = 256;    // workgroups a call aims for (one per CU)
 constexpr int kMergeChunk = 16;       // split partials read per round trip in the merge
 constexpr int kMergeSmall = 4;        // chunk used for the last few splits
 constexpr float kLog2e = 1.4426950408889634f;
@@ -150,21 +135,6 @@ __device__ __forceinline__ bool block_full(const Geometry& g, int lb) {
   return p1 <= g.a_end || (p0 >= g.r_start && p1 <= g.nc);
 }
 
-#if !ODA_FUSED_MERGE
-// Map a slot of the request dimension to a request id; false if the slot has
-// no selected request.
-__device__ __forceinline__ bool resolve_request(const AttnArgs& a, int slot, int& b) {
-  if (a.select == kSelList) {
-    if (slot >= a.n_work[0]) return false;
-    b = a.work_list[slot];
-    return b >= 0 && b < a.B;
-  }
-  b = slot;
-  if (a.select == kSelFlags) return a.flags[slot] != 0;
-  return true;
-}
-#endif
-
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
 // Requests with work in this call: the work list's count (at most the batch),
@@ -211,11 +181,11 @@ __device__ __forceinline__ bool request_of_rank(const AttnArgs& a, int rank, int
 // Blocks per split for this call.  With the automatic plan the split count
 // depends on how many requests are selected (known only on the device for
 // Full): enough splits that the selected requests give about
-// ODA_TARGET_GROUPS workgroups, at most max_splits (sized for one request).
+// kTargetGroups workgroups, at most max_splits (sized for one request).
 __device__ __forceinline__ int effective_bps(const AttnArgs& a, int active) {
   if (!a.dyn_splits) return a.bps;
   const int64_t units = (int64_t)max(active, 1) * a.L * a.Hkv;
-  const int64_t want = (ODA_TARGET_GROUPS + units - 1) / units;
+  const int64_t want = (kTargetGroups + units - 1) / units;
   const int s = (int)max((int64_t)1, min((int64_t)a.max_splits, want));
   const int bps = ((a.nvb_max + s - 1) / s + 1) & ~1;
   return uniform(max(bps, 2));
@@ -226,18 +196,10 @@ __device__ __forceinline__ bf16x8 load16(const uint16_t* p) {
 }
 // KV is read once per call: stream it with nontemporal loads.
 __device__ __forceinline__ bf16x8 stream16(const uint16_t* p) {
-#if ODA_KV_NONTEMPORAL
   return __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(p));
-#else
-  return *reinterpret_cast<const bf16x8*>(p);
-#endif
 }
 __device__ __forceinline__ u32x2 stream8(const uint16_t* p) {
-#if ODA_KV_NONTEMPORAL
   return __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
-#else
-  return *reinterpret_cast<const u32x2*>(p);
-#endif
 }
 __device__ __forceinline__ bf16x8 cat(u32x2 lo, u32x2 hi) {
   u32x4 t = {lo.x, lo.y, hi.x, hi.y};
@@ -684,7 +646,6 @@ void attn_split_kernel(AttnArgs a) {
   r.v_hi = min(v_end, r.v_lo + 2 * per_wave);
 
   run_unit<D, kLocal>(a, r, l, b, g, split, nsplit, smem);
-#if ODA_FUSED_MERGE
   if (nsplit == 1) return;   // finalised
   float* sm_zc = smem + kWaves * 32 + kWaves * G * D;
   // The last of the request's splits to finish merges them all.  The eight
@@ -692,23 +653,24 @@ void attn_split_kernel(AttnArgs a) {
   // published at device scope: every wavefront waits until its stores have
   // reached its XCD's L2, then one thread writes that L2 back (one release per
   // workgroup: a release per wavefront made one-layer Full calls over 32K
-  // positions ~40% slower) and takes a ticket.  The workgroup holding the last ticket
-  // drops stale cached lines (acquire), merges, and sets the count back to 0.
+  // positions ~40% slower) and takes a ticket.  The ticket counts modulo
+  // nsplit (a wrapping increment), so the last arrival sees nsplit - 1 and the
+  // word is back at 0 with no separate reset: even a request listed twice
+  // (2 nsplit arrivals) leaves it at 0 for later calls.  The workgroup holding
+  // the last ticket drops stale cached lines (acquire) and merges.
   __shared__ int last_split;
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   uint32_t* ticket = a.tickets + ((int64_t)l * a.B + b) * a.Hkv + g;
   if (threadIdx.x == 0) {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-    const uint32_t t = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t t = __builtin_amdgcn_atomic_inc32(ticket, (uint32_t)(nsplit - 1), __ATOMIC_RELAXED, "agent");
     last_split = (t == (uint32_t)(nsplit - 1)) ? 1 : 0;
   }
   __syncthreads();
   if (!last_split) return;
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   merge_unit<D>(a, l, b, g, nsplit, sm_zc, kWaves * 64);
-  if (threadIdx.x == 0) __hip_atomic_store(ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-#endif
 }
 
 // Batched Local with one split per unit and many units per CU: a work item is
@@ -755,30 +717,6 @@ void attn_local_layers_kernel(AttnArgs a) {
   }
 }
 
-#if !ODA_FUSED_MERGE
-// One workgroup per (layer, request slot, KV head) whose request has several
-// splits.
-template <int D>
-__global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(AttnArgs a) {
-  __shared__ float sm_zc[kMaxGroup];
-  int64_t unit = blockIdx.x;
-  const int g = (int)(unit % a.Hkv);
-  unit /= a.Hkv;
-  const int l = (int)(unit % a.L);
-  const int slot = (int)(unit / a.L);
-  if (slot >= a.B) return;
-  int b;
-  if (!resolve_request(a, slot, b)) return;
-  b = uniform(b);
-  const int n = uniform(a.seq_lens[b]);
-  if (!valid_len(a, n)) return;   // the split kernel wrote NaN rows
-  const Geometry geo = geometry(n, a.n_sink, a.window, a.has_cur);
-  const int bps = effective_bps(a, active_requests(a));
-  const int nsplit = max(1, (geo.nvb + bps - 1) / bps);
-  if (nsplit <= 1) return;   // finalized by the split kernel
-  merge_unit<D>(a, l, b, g, nsplit, sm_zc, kMergeThreads);
-}
-#endif
 
 // ---------------------------------------------------------------------------
 // host side
@@ -819,7 +757,7 @@ oda_status check_shape(const oda_attn_shape* s) {
 
 // Work decomposition.  One workgroup per (request, layer, KV head, split).
 // The automatic plan splits a request only as much as needed for the selected
-// requests to give the GPU about ODA_TARGET_GROUPS workgroups (one per CU).
+// requests to give the GPU about kTargetGroups workgroups (one per CU).
 // Local selects every request; Full's grid and workspace are sized for the
 // case of a single selected request (max_splits), and the kernels pick the
 // actual split count on the device (effective_bps).  The workspace size a
@@ -839,7 +777,7 @@ void make_plan(const oda_attn_shape* s, int n_sink, int window, int64_t selected
   int64_t bps = s->split_blocks;
   p->dyn = 0;
   if (bps == 0) {
-    const int64_t want = oda::ceil_div(ODA_TARGET_GROUPS, units_selected);
+    const int64_t want = oda::ceil_div(kTargetGroups, units_selected);
     // at least one block pair per wavefront
     const int64_t max_split = std::max<int64_t>(1, nvb / (2 * kWaves));
     const int64_t nsplit = std::max<int64_t>(1, std::min(want, max_split));
@@ -861,7 +799,7 @@ void make_plan(const oda_attn_shape* s, int n_sink, int window, int64_t selected
   const int64_t ml_bytes = oda::round_up(parts * 2 * 4, 256);
   // ticket words first: their place depends only on L * B * Hkv, so a
   // workspace stays valid across calls that differ in sinks or window
-  const int64_t t_bytes = ODA_FUSED_MERGE ? oda::round_up(units * 4, 256) : 0;
+  const int64_t t_bytes = oda::round_up(units * 4, 256);
   p->off_o = (size_t)t_bytes;
   p->off_ml = (size_t)(t_bytes + o_bytes);
   p->bytes = (size_t)(t_bytes + o_bytes + ml_bytes);
@@ -882,13 +820,13 @@ oda_status check_inputs(const oda_attn_inputs* in, const float* out) {
 }
 
 // Layers per work item of a Local call: the most (a divisor of L) that still
-// leave at least ODA_TARGET_GROUPS workgroups, when every unit has one split;
+// leave at least kTargetGroups workgroups, when every unit has one split;
 // 1 (the split kernel) otherwise.
 int layers_per_item(const oda_attn_shape* s, const Plan& plan) {
   if (plan.max_splits != 1) return 1;
   const int64_t per_layer = (int64_t)s->batch * s->num_kv_heads;
   for (int d = s->num_layers; d > 1; --d)
-    if (s->num_layers % d == 0 && (s->num_layers / d) * per_layer >= ODA_TARGET_GROUPS) return d;
+    if (s->num_layers % d == 0 && (s->num_layers / d) * per_layer >= kTargetGroups) return d;
   return 1;
 }
 
@@ -933,10 +871,6 @@ oda_status launch(const AttnArgs& args, const Plan& plan, hipStream_t stream) {
                   (int)(split_lds_floats(kMaxGroup, D) * 4));
   (void)hipGetLastError();
   hipLaunchKernelGGL((attn_split_kernel<D, kLocal>), dim3((unsigned)items), dim3(kWaves * 64), lds, stream, args);
-#if !ODA_FUSED_MERGE
-  if (plan.max_splits > 1)
-    hipLaunchKernelGGL(attn_merge_kernel<D>, dim3((unsigned)units), dim3(kMergeThreads), 0, stream, args);
-#endif
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return oda::fail(ODA_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ODA_OK;
@@ -969,7 +903,7 @@ oda_status run_attention(const oda_attn_shape* s, const oda_attn_inputs* in, boo
   a.lse = lse;
   a.part_o = plan.bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + plan.off_o) : nullptr;
   a.part_ml = plan.bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + plan.off_ml) : nullptr;
-  a.tickets = (plan.bytes != 0 && ODA_FUSED_MERGE != 0) ? static_cast<uint32_t*>(ws) : nullptr;
+  a.tickets = plan.bytes != 0 ? static_cast<uint32_t*>(ws) : nullptr;
   a.kv_layer_stride = s->num_blocks * s->num_kv_heads * kBlock * s->head_dim;
   a.max_len = s->max_seq_len;
   a.num_blocks = s->num_blocks;

@@ -247,3 +247,29 @@ def test_one_workspace_serves_many_calls(cur):
             assert np.all(o[:, 1] == 7.0)
         units = pb.L * pb.B * pb.Hkv
         assert int(ws[:4 * units].view(torch.int32).abs().sum().item()) == 0
+
+
+def test_repeated_list_entry_leaves_the_workspace_valid():
+    """A work list that names a request twice (a caller bug the gate never
+    produces) gives that request unspecified rows, but its merge tickets count
+    modulo the split count, so they return to zero: the other listed request
+    is correct, an unlisted one is untouched, and a normal call on the same
+    workspace afterwards matches the oracle."""
+    pb = AttnProblem(43, 2, 3, 8, 2, 128, [400, 230, 515], split_blocks=2)
+    P = pb.P
+    ws = torch.zeros(P.attn_workspace_size(pb.shape, 0, 0), dtype=torch.uint8, device="cuda")
+    units = pb.L * pb.B * pb.Hkv
+    out, lse = pb.new_out(7.0)
+    P.full_decode_attn(pb.shape, pb.inp, 0, None, dev_i32([2, 2, 0]), dev_i32([3]), out, lse, ws)
+    torch.cuda.synchronize()
+    assert int(ws[:4 * units].view(torch.int32).abs().sum().item()) == 0
+    o = out.cpu().numpy()
+    check_close(o[:, [0]], pb.oracle_full(requests=[0])[0][:, [0]])
+    assert np.all(o[:, 1] == 7.0)
+    out, lse = pb.new_out(7.0)
+    P.full_decode_attn(pb.shape, pb.inp, 0, None, dev_i32([1, 2]), dev_i32([2]), out, lse, ws)
+    torch.cuda.synchronize()
+    want = pb.oracle_full(requests=[1, 2])
+    _cmp(pb, (out, lse), want, requests=[1, 2])
+    assert np.all(out.cpu().numpy()[:, 0] == 7.0)
+    assert int(ws[:4 * units].view(torch.int32).abs().sum().item()) == 0
