@@ -1,6 +1,7 @@
-// Selected-state commit (App. A.5, commit equation): the chosen branch's
-// current-position K/V of every layer is appended to the paged cache, then
-// the request's length advances.
+// Selected-state commit (App. A.5, commit equation, and its single fused
+// cross-layer commit): the chosen branch's current-position K/V of every
+// layer is appended to the paged cache and the request's length advances, in
+// one launch.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -12,7 +13,8 @@ namespace {
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBlock = 16;
-constexpr int kThreads = 64;   // one wavefront: D/8 <= 16 threads work
+constexpr int kThreads = 1024;   // one workgroup per request
+constexpr int kInFlight = 4;     // (unit, 8-dim group) items each thread loads before it stores
 
 struct CommitArgs {
   uint16_t* k_cache;
@@ -30,41 +32,57 @@ struct CommitArgs {
   int32_t advance;
 };
 
-// One workgroup per (request, layer, KV head): thread t < D/8 moves dims
-// 8t..8t+7 of K (one 16-byte store into the [D/8][16][8] block) and of V
-// (eight 2-byte stores down the block's [D][16] column).  The lengths are
-// advanced by a second launch, so every copy reads the step's length.
-__global__ __launch_bounds__(kThreads) void commit_copy_kernel(CommitArgs a) {
-  int64_t unit = blockIdx.x;
-  const int g = (int)(unit % a.Hkv);
-  unit /= a.Hkv;
-  const int l = (int)(unit % a.L);
-  const int b = (int)(unit / a.L);
-  const int d8 = threadIdx.x;
-  if (d8 >= a.D / 8) return;
-  const int pos = a.seq_lens[b] - 1;
-  // a length or block-table entry outside the cache writes nothing
-  if (pos < 0 || pos >= a.MB * kBlock) return;
-  const int64_t blk = a.block_table[(int64_t)b * a.MB + pos / kBlock];
-  if (blk < 0 || blk >= a.NB) return;
+// The whole commit of one request in one launch: workgroup b reads its
+// length once, moves the selected candidate of every (layer, KV head) into
+// position n - 1 -- an item is 8 dims of one unit: one 16-byte store into the
+// K block's [D/8][16][8] layout and eight 2-byte stores down the V block's
+// [D][16] columns -- and, after a workgroup barrier (every thread has read the
+// length by then), advances the length.  A length or block-table entry
+// outside the cache writes nothing to the cache (the length still advances).
+__global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
+  const int b = blockIdx.x;
+  const int n = a.seq_lens[b];
+  const int pos = n - 1;
+  const bool in_table = pos >= 0 && pos < a.MB * kBlock;
+  const int64_t blk = in_table ? a.block_table[(int64_t)b * a.MB + pos / kBlock] : -1;
+  // uniform over the workgroup: a slot outside the cache is not written
+  const int items = (blk >= 0 && blk < a.NB) ? a.L * a.Hkv * (a.D / 8) : 0;
   const bool full = a.flags != nullptr && a.flags[b] != 0;
   const uint16_t* ks = full ? a.k_full : a.k_local;
   const uint16_t* vs = full ? a.v_full : a.v_local;
   const int slot = pos % kBlock;
-  const int64_t src = (((int64_t)l * a.B + b) * a.Hkv + g) * a.D + d8 * 8;
-  const int64_t dst = (int64_t)l * a.kv_layer_stride + (blk * a.Hkv + g) * kBlock * a.D;
-  const u32x4 kv = *reinterpret_cast<const u32x4*>(ks + src);
-  const u32x4 vv = *reinterpret_cast<const u32x4*>(vs + src);
-  *reinterpret_cast<u32x4*>(a.k_cache + dst + ((int64_t)d8 * kBlock + slot) * 8) = kv;
-  const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
+  const int groups = a.D / 8;
+  for (int i0 = threadIdx.x; i0 < items; i0 += kInFlight * kThreads) {
+    u32x4 kv[kInFlight], vv[kInFlight];
 #pragma unroll
-  for (int e = 0; e < 8; ++e)
-    a.v_cache[dst + (int64_t)(d8 * 8 + e) * kBlock + slot] = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
-}
-
-__global__ __launch_bounds__(256) void commit_advance_kernel(int32_t* seq_lens, int B) {
-  const int b = blockIdx.x * 256 + threadIdx.x;
-  if (b < B) seq_lens[b] += 1;
+    for (int u = 0; u < kInFlight; ++u) {
+      const int i = i0 + u * kThreads;
+      if (i < items) {
+        const int unit = i / groups, d8 = i - unit * groups;   // unit = l * Hkv + g
+        const int l = unit / a.Hkv, g = unit - l * a.Hkv;
+        const int64_t src = (((int64_t)l * a.B + b) * a.Hkv + g) * a.D + d8 * 8;
+        kv[u] = *reinterpret_cast<const u32x4*>(ks + src);
+        vv[u] = *reinterpret_cast<const u32x4*>(vs + src);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kInFlight; ++u) {
+      const int i = i0 + u * kThreads;
+      if (i < items) {
+        const int unit = i / groups, d8 = i - unit * groups;
+        const int l = unit / a.Hkv, g = unit - l * a.Hkv;
+        const int64_t dst = (int64_t)l * a.kv_layer_stride + (blk * a.Hkv + g) * kBlock * a.D;
+        *reinterpret_cast<u32x4*>(a.k_cache + dst + ((int64_t)d8 * kBlock + slot) * 8) = kv[u];
+        const uint32_t w[4] = {vv[u].x, vv[u].y, vv[u].z, vv[u].w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          a.v_cache[dst + (int64_t)(d8 * 8 + e) * kBlock + slot] = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
+      }
+    }
+  }
+  if (!a.advance) return;
+  __syncthreads();
+  if (threadIdx.x == 0) a.seq_lens[b] = n + 1;
 }
 
 }  // namespace
@@ -106,12 +124,9 @@ extern "C" oda_status oda_commit_kv(const oda_attn_shape* shape, uint16_t* k_cac
   a.NB = shape->num_blocks;
   a.advance = advance != 0;
   (void)hipGetLastError();
-  const int64_t units = (int64_t)shape->batch * shape->num_layers * shape->num_kv_heads;
-  if (units > 0x7fffffffLL) return oda::fail(ODA_ERR_SHAPE, "grid too large");
-  hipLaunchKernelGGL(commit_copy_kernel, dim3((unsigned)units), dim3(kThreads), 0, stream, a);
-  if (a.advance)
-    hipLaunchKernelGGL(commit_advance_kernel, dim3((unsigned)oda::ceil_div(shape->batch, 256)), dim3(256), 0, stream,
-                       seq_lens, shape->batch);
+  if ((int64_t)shape->num_layers * shape->num_kv_heads * (shape->head_dim / 8) > 0x7fffffffLL)
+    return oda::fail(ODA_ERR_SHAPE, "too many (layer, KV head) units");
+  hipLaunchKernelGGL(commit_kernel, dim3((unsigned)shape->batch), dim3(kThreads), 0, stream, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return oda::fail(ODA_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return oda::ok();
