@@ -19,7 +19,7 @@ and max); "warm" numbers run the K steps back to back.  Two launch modes:
 stacked (one call covers every layer of a group; the metric) and per-layer
 (one call per layer, eager and as a captured HIP graph; the realism check).
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--reps R] [--config llama3-8b] [--head paper|mlp]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--reps R] [--config mixed] [--head paper|mlp]
 
 Prints one JSON line: the headline value (µs per step at the recall rate
 nearest 0.1), the per-rate sweep for both recall heads, the per-layer launch
@@ -51,10 +51,14 @@ sys.path.insert(0, ROOT)
 METRIC = "decode-attn µs/step + achieved HBM GB/s vs always-Full, recall rate 0-100%"
 HBM_PEAK_GBS = 8000.0
 HEADLINE_RHO = 0.1
+FLAG_BORDER = 1e-4      # |score - tau| below this: a borderline decision (fp32 kernel vs fp64 oracle)
 ROOFLINE_REPS = 20
 ROOFLINE_KERNEL = "attn_split_kernel<128, false>"
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_20734_amd", "csrc", "attention.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "full_split_llama3-8b_traffic.txt")
+
+
+def traffic_file(workload: str) -> str:
+    return os.path.join(ROOT, "profiles", f"full_split_{workload}_traffic.txt")
 
 
 def source_sha256() -> str:
@@ -63,20 +67,24 @@ def source_sha256() -> str:
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def measured_traffic():
-    """HBM bytes per launch of the roofline kernel from the committed PMC summary,
-    or None if there is none or the kernel source changed since it was taken."""
-    if not os.path.exists(TRAFFIC_FILE):
+def measured_traffic(workload: str, bytes_per_launch: int):
+    """HBM bytes per launch of the roofline kernel from the committed PMC summary
+    of this workload, or None if there is none, if it was taken on another
+    launch size, or if the kernel source changed since it was taken."""
+    path = traffic_file(workload)
+    if not os.path.exists(path):
         return None
     vals = {}
-    with open(TRAFFIC_FILE) as f:
+    with open(path) as f:
         for line in f:
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
                 vals[k.strip()] = v.strip()
-    if vals.get("source_sha256") != source_sha256():
+    if vals.get("source_sha256") != source_sha256() or vals.get("workload_name") != workload:
         return None
     try:
+        if int(vals["algorithmic_bytes_per_launch"]) != int(bytes_per_launch):
+            return None
         return float(vals["traffic_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
@@ -279,6 +287,20 @@ class Bench:
         full = [P.prepare_full(s.shape, s.inp, s.stack.native_window, None, None, None, s.out, s.lse, s.ws_full)
                 for s in self.stacks]
         return [full] * self.K
+
+    def step_flags(self, tau, forced=None):
+        """The gate's flags for each of the K steps at one operating point
+        (the gate alone, outside any timed region): int32 [K][B]."""
+        torch = self.torch
+        B = self.wl.batch
+        out = torch.zeros((self.K, B), dtype=torch.int32, device=self.dev)
+        work = torch.zeros(B, dtype=torch.int32, device=self.dev)
+        n_work = torch.zeros(1, dtype=torch.int32, device=self.dev)
+        for t in range(self.K):
+            self.P.recall_gate(self.gate, B, self.h[t], self.e[t], self.l[t], tau,
+                               None if forced is None else forced[t], self.score, out[t], work, n_work, None,
+                               self.ws_gate)
+        return out.cpu().numpy()
 
     def scores(self):
         """Gate scores of all K steps (tau = +inf), for threshold calibration."""
@@ -670,17 +692,56 @@ def cpu_baseline(wl, head, seed, rho, budget_s=10.0, mem_cap=8e9):
     _CPU.clear()
     note = (f"K/V: seeded N(0,1) bf16 slabs tiled to the cache shape, {wl.batch} request(s), block table and "
             f"lengths as on the GPU; rho={rho} weighs Full; one gate evaluation ({head} head) for the batch")
-    return dict(value=one * 1e6, unit="us/step", cores=1, kind="oracle",
+    return dict(value=one * 1e6, unit="us/step", cores=1, kind="oracle", extrapolated=done < len(tasks),
                 sample=f"{done} of {len(tasks)} (layer, request) slices, Local + Full, fp64 NumPy, 1 thread"
                        + (", extrapolated to every slice in attended positions" if done < len(tasks) else "")
                        + "; " + note,
                 measured_s=t_gate + t_loc + t_full,
                 host_cpus=os.cpu_count(), affinity_cpus=len(os.sched_getaffinity(0)),
-                pool=dict(value=pooled * 1e6, unit="us/step", cores=cores, kind="oracle",
+                pool=dict(value=pooled * 1e6, unit="us/step", cores=cores, kind="oracle", extrapolated=m < len(tasks),
                           sample=f"{m} of {len(tasks)} slices over a {cores}-process pool (one thread each), "
                                  f"wall clock" + (", extrapolated to every slice in attended positions"
                                                   if m < len(tasks) else ""),
                           measured_s=w_loc + w_full))
+
+
+def oracle_gate_scores(wl, seed, steps):
+    """The fp64 oracle head's scores for every timed step's gate inputs (the
+    same seeded buffers the GPU reads), per head kind: [steps][B].  Part of
+    the CPU oracle leg (run before the GPU is touched); the sweep compares the
+    kernel's flags at every operating point with the decisions these scores
+    give."""
+    import oda_synth as S
+    from oracle import gate as OG
+    h, e, l_ = (x.astype(np.float64).reshape(steps * wl.batch, wl.d_model)
+                for x in S.gate_inputs(seed, steps, wl.batch, wl.d_model))
+    out = {}
+    for head in ("paper", "mlp"):
+        params = S.gate_params(seed, head, wl.d_model, wl.d_hidden)
+        if head == "paper":
+            sc = OG.paper_head_score(params, wl.d_model, wl.d_hidden, 1e-6, h, e, l_)
+        else:
+            sc = OG.mlp_score(params, wl.d_model, wl.d_hidden, l_)
+        out[head] = np.asarray(sc, dtype=np.float64).reshape(steps, wl.batch)
+    return out
+
+
+def flags_vs_oracle(gpu_flags, oracle_scores, tau, forced_np):
+    """Kernel flags of the K steps against the oracle's decisions (Full iff
+    score > tau, or the prescribed flag; nonfinite scores Full either way).
+    Decisions of a threshold whose fp64 score lies within FLAG_BORDER of it
+    are borderline: counted, and disagreements there reported apart."""
+    score = oracle_scores
+    fin = np.isfinite(score)
+    if forced_np is None:
+        want = (score > tau) | ~fin
+        border = fin & (np.abs(score - tau) < FLAG_BORDER)
+    else:
+        want = (forced_np != 0) | ~fin
+        border = np.zeros_like(want)
+    differ = gpu_flags.astype(bool) != want
+    return dict(decisions=int(want.size), borderline=int(border.sum()),
+                flag_mismatch=int((differ & ~border).sum()), borderline_differ=int((differ & border).sum()))
 
 
 def sweep_points(b, wl, args):
@@ -743,6 +804,10 @@ def run_sweep(b, wl, args, full_us, gated_only=False, points=None):
                    ratio=us / full_adj, ratio_first_full=us / full_us, ideal_ratio=nbytes / bytes_full)
         if pt["mode"] == "tau":
             ent["tau"] = pt["tau"]
+        oracle = getattr(b, "oracle_scores", None)
+        if oracle is not None:
+            ent["flags_vs_oracle"] = flags_vs_oracle(b.step_flags(pt["tau"], pt["forced"]), oracle[b.head],
+                                                     pt["tau"], pt["forced_np"])
         ent["hbm_frac"] = ent["GBps"] / HBM_PEAK_GBS
         ent["linearity"] = ent["ratio"] / ent["ideal_ratio"]
         if not args.no_warm:
@@ -752,7 +817,10 @@ def run_sweep(b, wl, args, full_us, gated_only=False, points=None):
         sweep.append(ent)
         log(f"[bench] {b.head} head {pt['mode']} rho={pt['rho']:.3f} (real {real:.3f}) {us:.1f} us/step "
             f"ratio {ent['ratio']:.3f} ideal {ent['ideal_ratio']:.3f} x{ent['linearity']:.2f} {ent['GBps']:.0f} GB/s"
-            + (" (retry on gated layers only)" if gated_only else ""))
+            + (" (retry on gated layers only)" if gated_only else "")
+            + (f"; flags vs oracle: {ent['flags_vs_oracle']['flag_mismatch']} mismatched, "
+               f"{ent['flags_vs_oracle']['borderline']} borderline of {ent['flags_vs_oracle']['decisions']}"
+               if "flags_vs_oracle" in ent else ""))
     return sweep
 
 
@@ -935,7 +1003,8 @@ def main():
     ap.add_argument("--steps", type=int, default=0, help="timed steps per repetition (default: the workload's)")
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--reps", type=int, default=3, help="repetitions of the K steps per operating point")
-    ap.add_argument("--config", default="llama3-8b")
+    ap.add_argument("--config", default="mixed",
+                    help="workload (default: the batched mixed-length stack, the largest single-GPU configuration)")
     ap.add_argument("--head", default="paper", choices=["paper", "mlp"])
     ap.add_argument("--seed", type=int, default=1234)
     ap.add_argument("--split-blocks", type=int, default=0)
@@ -969,17 +1038,21 @@ def main():
     pts_nominal = list(wl.bernoulli) if wl.bernoulli else list(wl.rhos)
     head_rho = min(pts_nominal, key=lambda r: abs(r - HEADLINE_RHO)) if pts_nominal else 1.0
 
-    # the CPU oracle first: its process pool forks before the GPU is touched
+    # the CPU oracle leg first: its process pool forks before the GPU is touched;
+    # it also scores every timed step's gate inputs with the fp64 oracle head
     cb = None
+    oracle_scores = None
     if not (args.no_cpu_baseline or args.roofline_only or args.loop_only):
         cb = cpu_baseline(wl, args.head, args.seed, head_rho)
         log(f"[bench] CPU oracle: {cb['value'] / 1e3:.1f} ms/step on 1 thread, {cb['pool']['value'] / 1e3:.1f} ms/step "
             f"on {cb['pool']['cores']} processes (host: {cb['host_cpus']} CPUs, {cb['affinity_cpus']} usable)")
+        oracle_scores = oracle_gate_scores(wl, args.seed, K)
 
     import torch
     b = Bench(wl, args.head, args.seed, K, args.split_blocks,
               growth=0 if (args.no_loop or args.roofline_only) else 16 * 8)
     P = b.P
+    b.oracle_scores = oracle_scores
     local_b, gate_b, full_b = bytes_for(wl, b.seq_host, None, args.head)
     bytes_full = sum(full_b)
 
@@ -1047,7 +1120,7 @@ def main():
     log(f"[bench] streaming-read ceiling: {ceil_full['GBps']:.0f} GB/s over {ceil_full['bytes'] / 1e9:.2f} GB, "
         f"{ceil_local['GBps']:.0f} GB/s over {ceil_local['bytes'] / 1e6:.0f} MB")
     roof = dict(bound="hbm", achieved=bytes_full / t_full_call / 1e3, peak=HBM_PEAK_GBS, unit="GB/s",
-                traffic=measured_traffic())
+                traffic=measured_traffic(wl.name, bytes_full))
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["kernel"] = ROOFLINE_KERNEL + " (oda_full_decode_attn, every request)"
     roof["bytes_per_launch"] = bytes_full
@@ -1064,8 +1137,11 @@ def main():
         "warmup": args.warmup, "reps": args.reps, "ms_per_step": round(value / 1e3, 6), "higher_is_better": False,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{wl.name}: {wl.num_layers} layers, B={wl.batch}, {wl.num_q_heads}q/{wl.num_kv_heads}kv "
-                               f"heads, D={wl.head_dim}, n={'/'.join(str(x) for x in nset[:4])}"
-                               f"{'...' if len(nset) > 4 else ''}, "
+                               f"heads, D={wl.head_dim}, "
+                               + (f"n~U[{wl.seq_range[0]},{wl.seq_range[1]}] (seeded; realised mean "
+                                  f"{float(b.seq_host.mean()):.0f}, KV {sum(full_b) / 1e9:.1f} GB)"
+                                  if wl.seq_range else f"n={'/'.join(str(x) for x in nset[:4])}"
+                                  f"{'...' if len(nset) > 4 else ''}") + ", "
                                f"W={wl.stacks[-1].local_window}, s={wl.stacks[-1].local_sink}, paged bf16 KV "
                                f"(block 16, permuted), {args.head} recall head {wl.d_model}->{wl.d_hidden}->1, "
                                f"{head_ent['mode'] + ' ' if head_ent else ''}rho={head_ent['rho'] if head_ent else 1.0}, "
