@@ -189,6 +189,23 @@ oda_status oda_recall_gate(const oda_gate_desc *gate, int32_t batch, const float
                            int64_t *recall_counter, void *workspace, size_t workspace_bytes,
                            hipStream_t stream);
 
+/* oda_recall_gate for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same computation and results, with the intermediate activations in a
+ * workspace the library holds itself -- a 16 MiB device array per GPU, set
+ * up on the first call on that GPU and kept until the process ends -- so the
+ * call takes no workspace argument and allocates nothing.  Returns
+ * ODA_ERR_WORKSPACE when oda_gate_workspace_size(gate, batch) exceeds 16 MiB
+ * (the App. A.2 head takes 28 * batch * dt bytes for three or more requests:
+ * up to 2,340 requests at dt = 256, 585 at dt = 1,024).  Every call on a GPU uses that GPU's one array: calls that may
+ * overlap in time on one GPU (other streams, other host threads) race and
+ * must be serialised by the caller.  The array's contents between calls do
+ * not matter (each call writes what it reads). */
+oda_status oda_recall_gate_static(const oda_gate_desc *gate, int32_t batch, const float *h_prev, const float *emb,
+                                  const float *h_local, float tau, const int32_t *forced, float *score,
+                                  int32_t *flags, int32_t *work_list, int32_t *n_work, int64_t *recall_counter,
+                                  hipStream_t stream);
+
 /* Full decode attention in the layers' native configuration (§2.1; App. A.5).
  * native_window == 0: S^F = all positions 0..n-1 (full-history layers);
  * native_window  > 0: the last native_window positions (natively

@@ -33,7 +33,8 @@ DENSE_PLAIN = 0
 DENSE_SWIGLU = 1
 
 EXPORTED = ("oda_attn_workspace_size", "oda_local_decode_attn", "oda_full_decode_attn",
-            "oda_gate_param_count", "oda_gate_workspace_size", "oda_recall_gate", "oda_commit_kv",
+            "oda_gate_param_count", "oda_gate_workspace_size", "oda_recall_gate", "oda_recall_gate_static",
+            "oda_commit_kv",
             "oda_dense_bf16", "oda_qk_norm_rope", "oda_embed_bf16", "oda_copy_rows", "oda_rms_norm_rows",
             "oda_argmax", "oda_stream_read", "oda_status_string", "oda_last_error")
 
@@ -91,6 +92,9 @@ _lib.oda_recall_gate.argtypes = [_P(GateDesc), ctypes.c_int32, ctypes.c_void_p, 
                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                  ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
 _lib.oda_recall_gate.restype = ctypes.c_int
+_lib.oda_recall_gate_static.argtypes = [_P(GateDesc), ctypes.c_int32, _V, _V, _V, ctypes.c_float, _V, _V, _V, _V, _V,
+                                        _V, _V]
+_lib.oda_recall_gate_static.restype = ctypes.c_int
 _lib.oda_commit_kv.argtypes = [_P(AttnShape), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                ctypes.c_int32, ctypes.c_void_p]
@@ -231,6 +235,14 @@ def recall_gate(gate: GateDesc, batch: int, h_prev, emb, h_local, tau: float, fo
     _check(_lib.oda_recall_gate(ctypes.byref(gate), batch, _ptr(h_prev), _ptr(emb), _ptr(h_local),
                                 float(tau), _ptr(forced), _ptr(score), _ptr(flags), _ptr(work_list),
                                 _ptr(n_work), _ptr(recall_counter), _ptr(workspace), wb, _stream(stream)))
+
+
+def recall_gate_static(gate: GateDesc, batch: int, h_prev, emb, h_local, tau: float, forced, score, flags, work_list,
+                       n_work, recall_counter, stream=None) -> None:
+    """oda_recall_gate with the library's own static workspace (no allocation)."""
+    _check(_lib.oda_recall_gate_static(ctypes.byref(gate), batch, _ptr(h_prev), _ptr(emb), _ptr(h_local),
+                                       float(tau), _ptr(forced), _ptr(score), _ptr(flags), _ptr(work_list),
+                                       _ptr(n_work), _ptr(recall_counter), _stream(stream)))
 
 
 def commit_kv(shape: Shape, k_cache, v_cache, block_table, seq_lens, k_local, v_local, k_full=None, v_full=None,

@@ -26,6 +26,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <utility>
 
@@ -717,35 +718,10 @@ void launch_fusion(const LinArgs& a, hipStream_t stream) {
   }
 }
 
-}  // namespace
-
-extern "C" oda_status oda_gate_param_count(int32_t kind, int32_t d_model, int32_t d_hidden, int64_t* count) {
-  if (count == nullptr) return oda::fail(ODA_ERR_NULL, "count is NULL");
-  if (d_model < 1 || d_hidden < 1) return oda::fail(ODA_ERR_SHAPE, "d_model and d_hidden must be >= 1");
-  if (kind == ODA_HEAD_PAPER) {
-    *count = paper_layout(d_model, d_hidden).total;
-  } else if (kind == ODA_HEAD_MLP) {
-    *count = (int64_t)d_hidden * d_model + 2 * (int64_t)d_hidden + 1;
-  } else {
-    return oda::fail(ODA_ERR_UNSUPPORTED, "unknown head kind %d", kind);
-  }
-  return oda::ok();
-}
-
-extern "C" oda_status oda_gate_workspace_size(const oda_gate_desc* gate, int32_t batch, size_t* bytes) {
-  oda_status st = check_gate(gate);
-  if (st != ODA_OK) return st;
-  if (bytes == nullptr) return oda::fail(ODA_ERR_NULL, "bytes is NULL");
-  if (batch < 1) return oda::fail(ODA_ERR_SHAPE, "batch must be >= 1");
-  *bytes = gate_ws_layout(gate->kind, batch, gate->d_hidden).bytes;
-  return oda::ok();
-}
-
-extern "C" oda_status oda_recall_gate(const oda_gate_desc* gate, int32_t batch, const float* h_prev,
-                                     const float* emb, const float* h_local, float tau, const int32_t* forced,
-                                     float* score, int32_t* flags, int32_t* work_list, int32_t* n_work,
-                                     int64_t* recall_counter, void* workspace, size_t workspace_bytes,
-                                     hipStream_t stream) {
+// Argument checks shared by both gate entry points (everything but the workspace).
+oda_status check_gate_call(const oda_gate_desc* gate, int32_t batch, const float* h_prev, const float* emb,
+                           const float* h_local, float tau, const float* score, const int32_t* flags,
+                           const int32_t* work_list, const int32_t* n_work) {
   oda_status st = check_gate(gate);
   if (st != ODA_OK) return st;
   if (batch < 1) return oda::fail(ODA_ERR_SHAPE, "batch must be >= 1");
@@ -758,12 +734,19 @@ extern "C" oda_status oda_recall_gate(const oda_gate_desc* gate, int32_t batch, 
   if (!oda::aligned(gate->params, 16) || !oda::aligned(h_local, 16) ||
       (paper && (!oda::aligned(h_prev, 16) || !oda::aligned(emb, 16))))
     return oda::fail(ODA_ERR_SHAPE, "params and gate inputs must be 16-byte aligned");
-  const GateWs ws = gate_ws_layout(gate->kind, batch, gate->d_hidden);
-  if (workspace == nullptr) return oda::fail(ODA_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", ws.bytes);
-  if (workspace_bytes < ws.bytes)
-    return oda::fail(ODA_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", workspace_bytes, ws.bytes);
-  if (!oda::aligned(workspace, 256)) return oda::fail(ODA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  return ODA_OK;
+}
 
+// Enqueue the head, the decision and the compaction, with the intermediate
+// activations in `workspace` (at least gate_ws_layout(...).bytes, 256-byte
+// aligned; every byte the kernels read there was written earlier in the same
+// call, so its contents on entry do not matter).
+oda_status run_gate(const oda_gate_desc* gate, int32_t batch, const float* h_prev, const float* emb,
+                    const float* h_local, float tau, const int32_t* forced, float* score, int32_t* flags,
+                    int32_t* work_list, int32_t* n_work, int64_t* recall_counter, void* workspace,
+                    hipStream_t stream) {
+  const bool paper = gate->kind == ODA_HEAD_PAPER;
+  const GateWs ws = gate_ws_layout(gate->kind, batch, gate->d_hidden);
   char* wsb = static_cast<char*>(workspace);
   const int d = gate->d_model, dt = gate->d_hidden;
   const float* P = gate->params;
@@ -910,5 +893,91 @@ extern "C" oda_status oda_recall_gate(const oda_gate_desc* gate, int32_t batch, 
   hipLaunchKernelGGL(gate_final_kernel, dim3(1), dim3((unsigned)final_threads), 0, stream, fa);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return oda::fail(ODA_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return oda::ok();
+}
+
+// Workspace of oda_recall_gate_static: a file-scope device array, one copy
+// per GPU, held until the process ends.  In host code its name is only a
+// stand-in for the symbol; its device address on the current GPU is looked up
+// once per device (kStaticDevices slots) and cached.
+constexpr size_t kStaticScratchBytes = (size_t)16 << 20;
+constexpr int kStaticDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+std::atomic<void*> g_scratch_ptr[kStaticDevices];
+
+oda_status static_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return oda::fail(ODA_ERR_HIP, "hipGetDevice failed: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kStaticDevices)
+    return oda::fail(ODA_ERR_UNSUPPORTED, "device %d: the static workspace serves devices 0..%d", dev,
+                     kStaticDevices - 1);
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    // threads racing here look up the same address and store the same value
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return oda::fail(ODA_ERR_HIP, "hipGetSymbolAddress of the static workspace failed: %s", hipGetErrorString(e));
+    g_scratch_ptr[dev].store(p, std::memory_order_release);
+  }
+  *ptr = p;
+  return ODA_OK;
+}
+
+}  // namespace
+
+extern "C" oda_status oda_recall_gate(const oda_gate_desc* gate, int32_t batch, const float* h_prev,
+                                     const float* emb, const float* h_local, float tau, const int32_t* forced,
+                                     float* score, int32_t* flags, int32_t* work_list, int32_t* n_work,
+                                     int64_t* recall_counter, void* workspace, size_t workspace_bytes,
+                                     hipStream_t stream) {
+  oda_status st = check_gate_call(gate, batch, h_prev, emb, h_local, tau, score, flags, work_list, n_work);
+  if (st != ODA_OK) return st;
+  const GateWs ws = gate_ws_layout(gate->kind, batch, gate->d_hidden);
+  if (workspace == nullptr) return oda::fail(ODA_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", ws.bytes);
+  if (workspace_bytes < ws.bytes)
+    return oda::fail(ODA_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", workspace_bytes, ws.bytes);
+  if (!oda::aligned(workspace, 256)) return oda::fail(ODA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  return run_gate(gate, batch, h_prev, emb, h_local, tau, forced, score, flags, work_list, n_work, recall_counter,
+                  workspace, stream);
+}
+
+extern "C" oda_status oda_recall_gate_static(const oda_gate_desc* gate, int32_t batch, const float* h_prev,
+                                            const float* emb, const float* h_local, float tau,
+                                            const int32_t* forced, float* score, int32_t* flags,
+                                            int32_t* work_list, int32_t* n_work, int64_t* recall_counter,
+                                            hipStream_t stream) {
+  oda_status st = check_gate_call(gate, batch, h_prev, emb, h_local, tau, score, flags, work_list, n_work);
+  if (st != ODA_OK) return st;
+  const GateWs ws = gate_ws_layout(gate->kind, batch, gate->d_hidden);
+  if (ws.bytes > kStaticScratchBytes)
+    return oda::fail(ODA_ERR_WORKSPACE, "this head and batch need %zu bytes of workspace; the static one holds %zu",
+                     ws.bytes, kStaticScratchBytes);
+  void* workspace = nullptr;
+  st = static_scratch(&workspace);
+  if (st != ODA_OK) return st;
+  return run_gate(gate, batch, h_prev, emb, h_local, tau, forced, score, flags, work_list, n_work, recall_counter,
+                  workspace, stream);
+}
+
+extern "C" oda_status oda_gate_param_count(int32_t kind, int32_t d_model, int32_t d_hidden, int64_t* count) {
+  if (count == nullptr) return oda::fail(ODA_ERR_NULL, "count is NULL");
+  if (d_model < 1 || d_hidden < 1) return oda::fail(ODA_ERR_SHAPE, "d_model and d_hidden must be >= 1");
+  if (kind == ODA_HEAD_PAPER) {
+    *count = paper_layout(d_model, d_hidden).total;
+  } else if (kind == ODA_HEAD_MLP) {
+    *count = (int64_t)d_hidden * d_model + 2 * (int64_t)d_hidden + 1;
+  } else {
+    return oda::fail(ODA_ERR_UNSUPPORTED, "unknown head kind %d", kind);
+  }
+  return oda::ok();
+}
+
+extern "C" oda_status oda_gate_workspace_size(const oda_gate_desc* gate, int32_t batch, size_t* bytes) {
+  oda_status st = check_gate(gate);
+  if (st != ODA_OK) return st;
+  if (bytes == nullptr) return oda::fail(ODA_ERR_NULL, "bytes is NULL");
+  if (batch < 1) return oda::fail(ODA_ERR_SHAPE, "batch must be >= 1");
+  *bytes = gate_ws_layout(gate->kind, batch, gate->d_hidden).bytes;
   return oda::ok();
 }
