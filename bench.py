@@ -222,6 +222,7 @@ class Bench:
             cands.append(c)
         scale = 1.0 / math.sqrt(wl.head_dim)
         seq0 = self.dseq.clone()
+        ws_commit = torch.zeros(P.commit_workspace_size(self.stacks[-1].shape), dtype=torch.uint8, device=self.dev)
         res = []
 
         def one_period(forced):
@@ -237,7 +238,7 @@ class Bench:
                                        st.out, st.lse, st.ws_full)
                 for i, (st, (kl, vl, kf, vf)) in enumerate(zip(self.stacks, cands)):
                     P.commit_kv(st.shape, st.k, st.v, self.dtable, self.dseq, kl[t], vl[t], kf[t], vf[t],
-                                self.flags, i == len(self.stacks) - 1)
+                                self.flags, i == len(self.stacks) - 1, ws_commit)
 
         for k in firsts:
             sched = np.stack([S.periodic_schedule(period, k)] * B, axis=1).astype(np.int32)

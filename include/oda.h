@@ -228,24 +228,35 @@ oda_status oda_full_decode_attn(const oda_attn_shape *shape, const oda_attn_inpu
                                 float *lse, void *workspace, size_t workspace_bytes,
                                 hipStream_t stream);
 
-/* Selected-state commit (App. A.5, commit equation C_t = C_{t-1} || dC_t^{b_t}):
- * for every layer l, request b and KV head g, copies the selected branch's
- * current-position K/V -- the Full candidate (k_full, v_full) if flags[b] != 0,
- * else the Local candidate (k_local, v_local) -- into position n_b - 1 of the
- * paged cache (block block_table[b][(n_b-1)/16], slot (n_b-1)%16, layouts
- * above), where n_b = seq_lens[b] is the step's attended count (the candidate
- * was supplied to the attention calls as k_cur/v_cur).  Then, if advance != 0,
+/* Bytes of workspace oda_commit_kv needs when it advances the lengths: one
+ * ticket word per request, rounded up to 256 bytes (host out).  Zero-fill it
+ * before its first use; every call leaves it zero again. */
+oda_status oda_commit_workspace_size(const oda_attn_shape *shape, size_t *bytes);
+
+/* Selected-state commit (App. A.5, commit equation C_t = C_{t-1} || dC_t^{b_t},
+ * and its single fused cross-layer commit): in one launch, for every layer l,
+ * request b and KV head g, copies the selected branch's current-position K/V
+ * -- the Full candidate (k_full, v_full) if flags[b] != 0, else the Local
+ * candidate (k_local, v_local) -- into position n_b - 1 of the paged cache
+ * (block block_table[b][(n_b-1)/16], slot (n_b-1)%16, layouts above), where
+ * n_b = seq_lens[b] is the step's attended count (the candidate was supplied
+ * to the attention calls as k_cur/v_cur).  Then, if advance != 0,
  * seq_lens[b] += 1, ready for the next step's candidate.
  *   k_local, v_local: bf16 [L][B][Hkv][D] (required)
  *   k_full, v_full:   NULL (both) = same as the Local candidate
  *   flags:            NULL = every request keeps Local
+ *   workspace:        required when advance != 0: >= oda_commit_workspace_size
+ *                     bytes, 256-byte aligned, zero-filled before first use
+ *                     (every call leaves it zero); ignored otherwise.  Calls
+ *                     that may overlap in time need separate workspaces.
  * Only shape->num_layers, batch, num_kv_heads, head_dim, block_size,
  * max_blocks_per_seq and num_blocks are used.  The caller guarantees that the
  * block holding position n_b - 1 is allocated in block_table. */
 oda_status oda_commit_kv(const oda_attn_shape *shape, uint16_t *k_cache, uint16_t *v_cache,
                          const int32_t *block_table, int32_t *seq_lens, const uint16_t *k_local,
                          const uint16_t *v_local, const uint16_t *k_full, const uint16_t *v_full,
-                         const int32_t *flags, int32_t advance, hipStream_t stream);
+                         const int32_t *flags, int32_t advance, void *workspace, size_t workspace_bytes,
+                         hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
  * The decoder around the hot path (the backbone f_theta of §2.1 that Local and

@@ -16,6 +16,7 @@ not been built that raises ImportError (there is no fallback path).
 _EXPORTS = ("HEAD_MLP", "HEAD_PAPER", "OdaError", "Shape", "attn_workspace_size", "full_decode_attn",
             "gate_desc", "gate_param_count", "gate_workspace_size", "inputs", "local_decode_attn",
             "recall_gate", "lib", "prepare_local", "prepare_full", "prepare_gate", "Call", "commit_kv", "prepare_commit",
+            "commit_workspace_size",
             "DENSE_PLAIN", "DENSE_SWIGLU", "dense_desc", "dense_bf16", "qk_norm_rope", "embed_bf16", "copy_rows",
             "argmax", "prepare_dense", "prepare_qk_norm_rope", "prepare_embed", "prepare_copy_rows",
             "prepare_argmax", "stream_read", "prepare_stream_read", "rms_norm_rows", "prepare_rms_norm_rows",

@@ -34,7 +34,7 @@ DENSE_SWIGLU = 1
 
 EXPORTED = ("oda_attn_workspace_size", "oda_local_decode_attn", "oda_full_decode_attn",
             "oda_gate_param_count", "oda_gate_workspace_size", "oda_recall_gate", "oda_recall_gate_static",
-            "oda_commit_kv",
+            "oda_commit_workspace_size", "oda_commit_kv",
             "oda_dense_bf16", "oda_qk_norm_rope", "oda_embed_bf16", "oda_copy_rows", "oda_rms_norm_rows",
             "oda_argmax", "oda_stream_read", "oda_status_string", "oda_last_error")
 
@@ -95,9 +95,11 @@ _lib.oda_recall_gate.restype = ctypes.c_int
 _lib.oda_recall_gate_static.argtypes = [_P(GateDesc), ctypes.c_int32, _V, _V, _V, ctypes.c_float, _V, _V, _V, _V, _V,
                                         _V, _V]
 _lib.oda_recall_gate_static.restype = ctypes.c_int
+_lib.oda_commit_workspace_size.argtypes = [_P(AttnShape), _P(ctypes.c_size_t)]
+_lib.oda_commit_workspace_size.restype = ctypes.c_int
 _lib.oda_commit_kv.argtypes = [_P(AttnShape), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-                               ctypes.c_int32, ctypes.c_void_p]
+                               ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
 _lib.oda_commit_kv.restype = ctypes.c_int
 _lib.oda_dense_bf16.argtypes = [_P(DenseDesc), ctypes.c_int32, _V, _V, _V, _V, _V, _V]
 _lib.oda_dense_bf16.restype = ctypes.c_int
@@ -245,11 +247,19 @@ def recall_gate_static(gate: GateDesc, batch: int, h_prev, emb, h_local, tau: fl
                                        _ptr(n_work), _ptr(recall_counter), _stream(stream)))
 
 
+def commit_workspace_size(shape: Shape) -> int:
+    out = ctypes.c_size_t(0)
+    _check(_lib.oda_commit_workspace_size(ctypes.byref(shape.c()), ctypes.byref(out)))
+    return out.value
+
+
 def commit_kv(shape: Shape, k_cache, v_cache, block_table, seq_lens, k_local, v_local, k_full=None, v_full=None,
-              flags=None, advance: bool = True, stream=None) -> None:
+              flags=None, advance: bool = True, workspace=None, workspace_bytes: int | None = None,
+              stream=None) -> None:
     _check(_lib.oda_commit_kv(ctypes.byref(shape.c()), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
                               _ptr(seq_lens), _ptr(k_local), _ptr(v_local), _ptr(k_full), _ptr(v_full),
-                              _ptr(flags), 1 if advance else 0, _stream(stream)))
+                              _ptr(flags), 1 if advance else 0, _ptr(workspace),
+                              _nbytes(workspace, workspace_bytes), _stream(stream)))
 
 
 def dense_desc(in_features: int, out_features: int, mode: int, weight, norm_gain=None,
@@ -346,12 +356,14 @@ def prepare_gate(gate: GateDesc, batch: int, h_prev, emb, h_local, tau: float, f
 
 
 def prepare_commit(shape: Shape, k_cache, v_cache, block_table, seq_lens, k_local, v_local, k_full=None,
-                   v_full=None, flags=None, advance: bool = True, stream=None) -> Call:
+                   v_full=None, flags=None, advance: bool = True, workspace=None, workspace_bytes: int | None = None,
+                   stream=None) -> Call:
     cs = shape.c()
     args = (ctypes.byref(cs), _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(seq_lens), _ptr(k_local),
-            _ptr(v_local), _ptr(k_full), _ptr(v_full), _ptr(flags), 1 if advance else 0, _stream(stream))
+            _ptr(v_local), _ptr(k_full), _ptr(v_full), _ptr(flags), 1 if advance else 0, _ptr(workspace),
+            _nbytes(workspace, workspace_bytes), _stream(stream))
     return Call(_lib.oda_commit_kv, args, (cs, k_cache, v_cache, block_table, seq_lens, k_local, v_local, k_full,
-                                          v_full, flags))
+                                          v_full, flags, workspace))
 
 
 def prepare_dense(desc: DenseDesc, batch: int, x, residual, y, work_list=None, n_work=None, stream=None) -> Call:

@@ -111,6 +111,7 @@ class Decoder:
                                     dtype=torch.uint8, device=dev)
         self.ws_full = torch.zeros(max(256, P.attn_workspace_size(self.attn_shape, 0, 0)), dtype=torch.uint8,
                                    device=dev)
+        self.ws_commit = torch.zeros(P.commit_workspace_size(self.commit_shape()), dtype=torch.uint8, device=dev)
         self.scale = 1.0 / math.sqrt(D)
         w = weights
         self.d_qkv = [P.dense_desc(d, s.qkv_dim, P.DENSE_PLAIN, w["w_qkv"][l], w["attn_norm"][l], s.rms_eps)
@@ -156,7 +157,7 @@ class Decoder:
                 P.prepare_dense(self.d_vocab, B, self.h_prev, None, self.logits),
                 P.prepare_argmax(B, s.vocab, self.logits, self.next_token),
                 P.prepare_commit(self.commit_shape(), self.k_cache, self.v_cache, self.table, self.seq_lens,
-                                 self.k_loc, self.v_loc, k_full, v_full, flags, True)]
+                                 self.k_loc, self.v_loc, k_full, v_full, flags, True, self.ws_commit)]
 
     def commit_shape(self) -> P.Shape:
         a = self.attn_shape

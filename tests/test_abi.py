@@ -148,10 +148,12 @@ def test_commit_rejects_bad_arguments(L):
         a = dict(args)
         a.update(kw)
         L.commit_kv(shape, a["k_cache"], a["v_cache"], a["table"], a["seq"], a["kl"], a["vl"], a.get("kf"),
-                    a.get("vf"), None, True, stream=0)
+                    a.get("vf"), None, a.get("advance", True), a.get("ws", 0x8000), a.get("wb", 256), stream=0)
 
+    assert L.commit_workspace_size(s) == 256
+    assert L.commit_workspace_size(_shape(L, batch=65)) == 512
     for kw, status in [(dict(k_cache=None), -1), (dict(kl=None), -1), (dict(kf=0x7000), -1),
-                       (dict(kl=0x5008), -2)]:
+                       (dict(kl=0x5008), -2), (dict(ws=None), -4), (dict(wb=255), -4), (dict(ws=0x8010), -4)]:
         with pytest.raises(L.OdaError) as e:
             call(kw)
         assert e.value.status == status, (kw, e.value)

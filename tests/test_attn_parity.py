@@ -273,3 +273,41 @@ def test_repeated_list_entry_leaves_the_workspace_valid():
     _cmp(pb, (out, lse), want, requests=[1, 2])
     assert np.all(out.cpu().numpy()[:, 0] == 7.0)
     assert int(ws[:4 * units].view(torch.int32).abs().sum().item()) == 0
+
+
+@pytest.mark.parametrize("cur", [False, True])
+def test_selection_sizes_on_one_workspace(cur):
+    """Full calls over device-side selections of 0, 1, 5, 11 and 12 of 12
+    requests (4 layers, 8 KV heads: 384 units, automatic and forced split-K)
+    and a flags selection, on one workspace: each matches the oracle on the
+    selected rows, leaves the others untouched, and leaves the ticket words
+    zero."""
+    g = np.random.default_rng(91)
+    seq = g.integers(1, 900, size=12)
+    seq[[2, 7]] = [1, 2000]
+    for split_blocks in (0, 4):
+        pb = AttnProblem(91 + split_blocks, 4, 12, 32, 8, 64, seq.tolist(), cur=cur, split_blocks=split_blocks)
+        P = pb.P
+        ws = torch.zeros(max(256, P.attn_workspace_size(pb.shape, 0, 0)), dtype=torch.uint8, device="cuda")
+        units = pb.L * pb.B * pb.Hkv
+        for sel in ([], [7], [11, 0, 2, 7, 5], [b for b in range(12) if b != 4], list(range(12)), "flags"):
+            out, lse = pb.new_out(-7.0)
+            if sel == "flags":
+                fl = (np.arange(12) % 3 == 1).astype(np.int32)
+                rows = list(np.flatnonzero(fl))
+                P.full_decode_attn(pb.shape, pb.inp, 0, dev_i32(fl), None, None, out, lse, ws)
+            else:
+                rows = sel
+                wl = np.zeros(12, np.int32)
+                wl[:len(sel)] = sel
+                P.full_decode_attn(pb.shape, pb.inp, 0, None, dev_i32(wl), dev_i32([len(sel)]), out, lse, ws)
+            torch.cuda.synchronize()
+            assert int(ws[:4 * units].view(torch.int32).abs().sum().item()) == 0, (split_blocks, sel)
+            o, ls = out.cpu().numpy(), lse.cpu().numpy()
+            if rows:
+                ref = pb.oracle_full(0, requests=rows)
+                for b in rows:
+                    check_close(o[:, b], ref[0][:, b], what=f"split {split_blocks} sel {sel} request {b}")
+                    assert np.max(np.abs(ls[:, b] - ref[1][:, b])) <= LSE_ABS
+            for b in set(range(12)) - set(rows):
+                assert np.all(o[:, b] == -7.0) and np.all(ls[:, b] == -7.0)

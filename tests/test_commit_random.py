@@ -34,9 +34,10 @@ def test_random_commits(seed):
     vf = S.normal_bf16(S.rng(6200 + seed, S.STREAM_VCUR), (L, B, Hkv, D))
     dk, dv, dseq = dev_u16(k), dev_u16(v), dev_i32(seq)
     shape = P.Shape(L, B, Hkv, Hkv, D, mb, int(seq.max()), nb)
+    ws = torch.zeros(P.commit_workspace_size(shape), dtype=torch.uint8, device="cuda")
     P.commit_kv(shape, dk, dv, dev_i32(table), dseq, dev_u16(kl), dev_u16(vl),
                 dev_u16(kf) if with_full else None, dev_u16(vf) if with_full else None,
-                dev_i32(flags) if with_full else None, advance)
+                dev_i32(flags) if with_full else None, advance, ws)
     torch.cuda.synchronize()
     hk, hv, hseq = k.copy(), v.copy(), seq.copy()
     sel = flags if with_full else np.zeros(B, np.int32)
@@ -44,3 +45,4 @@ def test_random_commits(seed):
     assert np.array_equal(dk.cpu().numpy().view(np.uint16), hk)
     assert np.array_equal(dv.cpu().numpy().view(np.uint16), hv)
     assert dseq.cpu().numpy().tolist() == (hseq if advance else seq).tolist()
+    assert int(ws.sum().item()) == 0      # the tickets are back at zero

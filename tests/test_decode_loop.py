@@ -47,6 +47,7 @@ def test_decode_loop_with_commit(D, G):
     ws_l = torch.zeros(max(1, P.attn_workspace_size(shape, s, W)), dtype=torch.uint8, device="cuda")
     ws_f = torch.zeros(max(1, P.attn_workspace_size(shape, 0, 0)), dtype=torch.uint8, device="cuda")
     ws_g = torch.zeros(P.gate_workspace_size(gate, B), dtype=torch.uint8, device="cuda")
+    ws_c = torch.zeros(P.commit_workspace_size(shape), dtype=torch.uint8, device="cuda")
     score = torch.empty(B, device="cuda")
     flags = torch.empty(B, dtype=torch.int32, device="cuda")
     wl = torch.empty(B, dtype=torch.int32, device="cuda")
@@ -63,7 +64,7 @@ def test_decode_loop_with_commit(D, G):
         P.local_decode_attn(shape, inp_l, s, W, out, lse, ws_l)
         P.recall_gate(gate, B, dh[t], de[t], dhl[t], 0.0, dforced[t], score, flags, wl, nw, ctr, ws_g)
         P.full_decode_attn(shape, inp_f, 0, None, wl, nw, out, lse, ws_f)
-        P.commit_kv(shape, dk, dv, dtab, dseq, dkl[t], dvl[t], dkf[t], dvf[t], flags, True)
+        P.commit_kv(shape, dk, dv, dtab, dseq, dkl[t], dvl[t], dkf[t], dvf[t], flags, True, ws_c)
         torch.cuda.synchronize()
 
         ref_l = OA.decode_attention(q_all[t], hk, hv, table, hseq, lambda n: OA.local_set(n, s, W), scale,

@@ -40,6 +40,7 @@ def test_graph_replay_matches_eager():
     ws_l = torch.zeros(max(256, P.attn_workspace_size(shape, s, W)), dtype=torch.uint8, device="cuda")
     ws_f = torch.zeros(max(256, P.attn_workspace_size(shape, 0, 0)), dtype=torch.uint8, device="cuda")
     ws_g = torch.zeros(P.gate_workspace_size(gate, B), dtype=torch.uint8, device="cuda")
+    ws_c = torch.zeros(P.commit_workspace_size(shape), dtype=torch.uint8, device="cuda")
     score = torch.empty(B, device="cuda")
     flags = torch.empty(B, dtype=torch.int32, device="cuda")
     wl = torch.empty(B, dtype=torch.int32, device="cuda")
@@ -56,7 +57,7 @@ def test_graph_replay_matches_eager():
             P.recall_gate(gate, B, h[t], e[t], hl[t], 0.0, forced[t], score, flags, wl, nw, ctr, ws_g)
             P.full_decode_attn(shape, P.inputs(q[t], dk, dv, dtab, dseq, scale, kf[t], vf[t]), 0, None, wl, nw,
                                outs[t], lses[t], ws_f)
-            P.commit_kv(shape, dk, dv, dtab, dseq, kl[t], vl[t], kf[t], vf[t], flags, True)
+            P.commit_kv(shape, dk, dv, dtab, dseq, kl[t], vl[t], kf[t], vf[t], flags, True, ws_c)
 
     def reset():
         dk.copy_(k0)

@@ -77,7 +77,8 @@ def test_commit_writes_nothing_for_bad_lengths_or_entries():
     tab[2, (40 - 1) // 16] = nb + 1      # request 2's slot block is out of range
     dseq = dev_i32([0, 17, 40, 4 * 16 + 1])   # request 0: length 0; request 3: beyond the table
     shape = P.Shape(L, B, 8, Hkv, D, 4, 64, nb)
-    P.commit_kv(shape, dk, dv, dev_i32(tab), dseq, dev_u16(kl), dev_u16(vl))
+    ws = torch.zeros(P.commit_workspace_size(shape), dtype=torch.uint8, device="cuda")
+    P.commit_kv(shape, dk, dv, dev_i32(tab), dseq, dev_u16(kl), dev_u16(vl), workspace=ws)
     torch.cuda.synchronize()
     hk, hv = k.copy(), v.copy()
     pos = 16                              # request 1 (the only valid one) writes position 16
