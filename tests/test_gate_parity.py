@@ -77,7 +77,11 @@ def _check(g, h, e, l, tau, forced=None):
                                          # wavefront: unsplit blocks (these once ran the split kernel of
                                          # another width)
                                          ("paper", 1732, 192, 1), ("paper", 512, 384, 2), ("paper", 300, 96, 1),
-                                         ("paper", 64, 12, 2)])
+                                         ("paper", 64, 12, 2),
+                                         # 40 and 64 requests (several batch tiles), a few requests with short or
+                                         # ragged rows
+                                         ("paper", 1732, 192, 40), ("paper", 4096, 256, 64), ("paper", 100, 32, 4),
+                                         ("paper", 4100, 64, 17)])
 def test_scores_and_flags(kind, d, dh, B):
     g = Gate(kind, d, dh, B)
     h, e, l = (x[0] for x in S.gate_inputs(3, 1, B, d))
@@ -150,3 +154,23 @@ def test_equal_score_and_threshold_stays_local():
     sc2, fl, _, _ = g.run(h, e, l, float(sc[2]))
     assert np.array_equal(sc, sc2)          # deterministic
     assert fl[2] == 0
+
+
+def test_one_workspace_serves_heads_of_any_shape():
+    """Every byte a gate call reads from its workspace it wrote earlier in the
+    same call: one workspace, sized for the largest call and left holding the
+    previous call's activations, serves heads of different batches, widths and
+    launch paths in turn, each giving the results of a fresh workspace."""
+    P = need_gpu()
+    shapes = [("paper", 4096, 256, 32), ("paper", 4096, 256, 1), ("paper", 512, 64, 5), ("mlp", 4096, 256, 8),
+              ("paper", 1024, 128, 64), ("paper", 4096, 256, 32)]
+    gates = [Gate(kind, d, dh, B, seed=60 + i) for i, (kind, d, dh, B) in enumerate(shapes)]
+    shared = torch.zeros(max(g.ws.numel() for g in gates), dtype=torch.uint8, device="cuda")
+    for i, g in enumerate(gates):
+        h, e, l = (x[0] for x in S.gate_inputs(70 + i, 1, g.B, g.d))
+        fresh = g.run(h, e, l, 0.0)
+        own = g.ws
+        g.ws = shared
+        again = g.run(h, e, l, 0.0)
+        g.ws = own
+        assert np.array_equal(fresh[0], again[0]) and np.array_equal(fresh[1], again[1]), shapes[i]

@@ -1,8 +1,11 @@
 """Whole-step HIP graph: a period of decode steps (Local -> gate -> Full ->
 commit, per step) captured once and replayed, against the same steps run
-eagerly from the same state.  Replays are separated by eager work and host
-synchronisation, and every replay is checked (outputs of every step, the
-final caches, lengths and recall counter must be bit-identical)."""
+eagerly from the same state and against the fp64 oracle's replay of the
+period (its own attention, selection and commit on host copies).  Replays are
+separated by eager work and host synchronisation, and every replay is checked:
+each step's outputs against the oracle within the attention bar, and outputs,
+final caches, lengths and recall counter bit-identical to the eager run (the
+caches and lengths also equal the oracle's bit for bit)."""
 import math
 
 import numpy as np
@@ -10,12 +13,15 @@ import pytest
 import torch
 
 import oda_synth as S
-from harness import dev_f32, dev_i32, dev_u16, need_gpu
+from harness import LSE_ABS, check_close, dev_f32, dev_i32, dev_u16, need_gpu
+from oracle import attention as OA
+from oracle import step as OS
 
 pytestmark = pytest.mark.gpu
 
 
-def test_graph_replay_matches_eager():
+@pytest.mark.parametrize("dt", [16, 64])      # two tower widths
+def test_graph_replay_matches_eager(dt):
     P = need_gpu()
     L, B, Hkv, G, D, T = 2, 3, 2, 4, 128, 8
     Hq = Hkv * G
@@ -29,8 +35,10 @@ def test_graph_replay_matches_eager():
     sched = np.stack([S.periodic_schedule(T, 2)] * B, axis=1).astype(np.int32)   # first 2 of every T -> Full
     forced = dev_i32(sched)
     d = 64
-    gate = P.gate_desc(P.HEAD_PAPER, d, 16, dev_f32(S.gate_params(4, "paper", d, 16)))
+    gate = P.gate_desc(P.HEAD_PAPER, d, dt, dev_f32(S.gate_params(4, "paper", d, dt)))
     h, e, hl = (dev_f32(x) for x in S.gate_inputs(4, T, B, d))
+    q_h = S.normal_bf16(S.rng(2, S.STREAM_Q), (T, L, B, Hq, D))
+    cand_h = [S.normal_bf16(S.rng(3 + i, S.STREAM_KCUR), (T, L, B, Hkv, D)) for i in range(4)]
     shape = P.Shape(L, B, Hq, Hkv, D, mb, int(seq0.max()) + 4 * T, nb, 4)
     k0, v0 = dev_u16(k), dev_u16(v)
     dk, dv = k0.clone(), v0.clone()
@@ -67,9 +75,36 @@ def test_graph_replay_matches_eager():
         outs.zero_()
         lses.zero_()
 
+    # the oracle's replay of the period: Local with the Local candidate, Full
+    # with the Full candidate for the scheduled requests, the selected rows,
+    # then the commit of the selected candidates
+    hk, hv, hseq = k.copy(), v.copy(), seq0.copy()
+    want = []
+    for t in range(T):
+        loc = OA.decode_attention(q_h[t], hk, hv, table, hseq, lambda n: OA.local_set(n, s, W), scale,
+                                  k_cur=cand_h[0][t], v_cur=cand_h[1][t])
+        full = OA.decode_attention(q_h[t], hk, hv, table, hseq, OA.full_set, scale, k_cur=cand_h[2][t],
+                                   v_cur=cand_h[3][t])
+        o, l_ = loc[0].copy(), loc[1].copy()
+        for b in np.flatnonzero(sched[t]):
+            o[:, b], l_[:, b] = full[0][:, b], full[1][:, b]
+        want.append((o, l_))
+        OS.commit(hk, hv, table, hseq, cand_h[0][t], cand_h[1][t], cand_h[2][t], cand_h[3][t], sched[t])
+
+    def check_against_oracle(tag):
+        o_all, l_all = outs.cpu().numpy(), lses.cpu().numpy()
+        for t in range(T):
+            check_close(o_all[t], want[t][0], what=f"{tag} step {t}")
+            assert np.max(np.abs(l_all[t] - want[t][1])) <= LSE_ABS
+        assert np.array_equal(dk.cpu().numpy().view(np.uint16), hk)
+        assert np.array_equal(dv.cpu().numpy().view(np.uint16), hv)
+        assert dseq.cpu().numpy().tolist() == hseq.tolist()
+        assert int(ctr.item()) == int(sched.sum())
+
     reset()
     period()                     # eager reference (also warms up every kernel)
     torch.cuda.synchronize()
+    check_against_oracle("eager")
     ref = [x.clone() for x in (outs, lses, dk, dv, dseq, ctr)]
     assert int(ctr.item()) == 2 * B
 
@@ -86,4 +121,5 @@ def test_graph_replay_matches_eager():
         got = (outs, lses, dk, dv, dseq, ctr)
         for a, b_ in zip(got, ref):
             assert torch.equal(a, b_), f"replay {rep} differs from eager"
+        check_against_oracle(f"replay {rep}")
         _ = (outs * 2).sum().item()          # unrelated eager work between replays
