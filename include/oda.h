@@ -49,7 +49,16 @@
  *            K(pos, d) = k_cache[l][blk][g][d/8][pos%16][d%8]
  *   v_cache  bf16 [L][num_blocks][Hkv][D][16]
  *            paged values, dims-major:  V(pos, d) = v_cache[l][blk][g][d][pos%16]
- *            where blk = block_table[b][pos/16]
+ *            where blk = block_table[b][pos/16]; layer l starts layer_stride_kv
+ *            elements after layer l-1 (dense by default)
+ *   (Every 16-byte lane load of K is one matrix-core operand fragment and a
+ *   wavefront's load instruction reads 1 KiB contiguous; V needs no transpose.
+ *   Blocks stored position-major, [16][D] for both K and V as many paged
+ *   caches keep them, measured 55% slower on this hardware -- Full over the
+ *   32-layer 32,768-position stack 626 -> 970..990 us, Local 28 -> 41..44 us --
+ *   because each K load instruction then touches 16 separate half lines and V
+ *   must be transposed (through LDS or 2-byte gathers); the library does not
+ *   take that layout.)
  *   k_cur, v_cur  bf16 [L][B][Hkv][D]  (optional) the current token's candidate
  *            K/V, not yet committed to the cache (App. A.5)
  *   out      fp32 [L][B][Hq][D];  lse fp32 [L][B][Hq]  (natural log)
@@ -91,6 +100,10 @@ typedef struct {
   int32_t split_blocks;       /* KV blocks per split-K work item (one workgroup
                                  each): 0 = automatic, otherwise an even number >= 2 */
   int32_t reserved;           /* must be 0                                        */
+  int64_t layer_stride_kv;    /* elements between layers in k_cache / v_cache:
+                                 0 = num_blocks * Hkv * 16 * D (dense); else at
+                                 least that and a multiple of 8 (e.g. one
+                                 allocation holding several layer groups)       */
 } oda_attn_shape;
 
 /* Inputs of one attention call (host struct holding device pointers). */

@@ -52,7 +52,7 @@ class AttnShape(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("block_size", ctypes.c_int32),
                 ("max_blocks_per_seq", ctypes.c_int32), ("max_seq_len", ctypes.c_int32),
                 ("num_blocks", ctypes.c_int64), ("split_blocks", ctypes.c_int32),
-                ("reserved", ctypes.c_int32)]
+                ("reserved", ctypes.c_int32), ("layer_stride_kv", ctypes.c_int64)]
 
 
 class AttnInputs(ctypes.Structure):
@@ -169,11 +169,12 @@ class Shape:
     num_blocks: int
     split_blocks: int = 0
     block_size: int = 16
+    layer_stride_kv: int = 0
 
     def c(self) -> AttnShape:
         return AttnShape(self.num_layers, self.batch, self.num_q_heads, self.num_kv_heads, self.head_dim,
                          self.block_size, self.max_blocks_per_seq, self.max_seq_len, self.num_blocks,
-                         self.split_blocks, 0)
+                         self.split_blocks, 0, self.layer_stride_kv)
 
 
 def inputs(q, k_cache, v_cache, block_table, seq_lens, scale, k_cur=None, v_cur=None) -> AttnInputs:

@@ -752,6 +752,10 @@ oda_status check_shape(const oda_attn_shape* s) {
   if (s->split_blocks != 0 && (s->split_blocks < 2 || (s->split_blocks & 1)))
     return oda::fail(ODA_ERR_SHAPE, "split_blocks %d: 0 or an even number >= 2", s->split_blocks);
   if (s->reserved != 0) return oda::fail(ODA_ERR_SHAPE, "reserved must be 0");
+  const int64_t dense = s->num_blocks * s->num_kv_heads * kBlock * s->head_dim;
+  if (s->layer_stride_kv != 0 && (s->layer_stride_kv < dense || s->layer_stride_kv % 8 != 0))
+    return oda::fail(ODA_ERR_SHAPE, "layer_stride_kv %lld: 0, or a multiple of 8 >= %lld", (long long)s->layer_stride_kv,
+                     (long long)dense);
   return ODA_OK;
 }
 
@@ -904,7 +908,7 @@ oda_status run_attention(const oda_attn_shape* s, const oda_attn_inputs* in, boo
   a.part_o = plan.bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + plan.off_o) : nullptr;
   a.part_ml = plan.bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + plan.off_ml) : nullptr;
   a.tickets = plan.bytes != 0 ? static_cast<uint32_t*>(ws) : nullptr;
-  a.kv_layer_stride = s->num_blocks * s->num_kv_heads * kBlock * s->head_dim;
+  a.kv_layer_stride = s->layer_stride_kv != 0 ? s->layer_stride_kv : s->num_blocks * s->num_kv_heads * kBlock * s->head_dim;
   a.max_len = s->max_seq_len;
   a.num_blocks = s->num_blocks;
   a.L = s->num_layers;

@@ -98,6 +98,10 @@ oda_status check_commit_shape(const oda_attn_shape* shape) {
   if (shape->head_dim != 64 && shape->head_dim != 128)
     return oda::fail(ODA_ERR_UNSUPPORTED, "head_dim %d not in {64, 128}", shape->head_dim);
   if (shape->block_size != kBlock) return oda::fail(ODA_ERR_UNSUPPORTED, "block_size %d != 16", shape->block_size);
+  const int64_t dense = shape->num_blocks * shape->num_kv_heads * kBlock * shape->head_dim;
+  if (shape->layer_stride_kv != 0 && (shape->layer_stride_kv < dense || shape->layer_stride_kv % 8 != 0))
+    return oda::fail(ODA_ERR_SHAPE, "layer_stride_kv %lld: 0, or a multiple of 8 >= %lld",
+                     (long long)shape->layer_stride_kv, (long long)dense);
   return ODA_OK;
 }
 
@@ -145,7 +149,8 @@ extern "C" oda_status oda_commit_kv(const oda_attn_shape* shape, uint16_t* k_cac
   a.v_full = v_full ? v_full : v_local;
   a.flags = flags;
   a.tickets = advance != 0 ? static_cast<uint32_t*>(workspace) : nullptr;
-  a.kv_layer_stride = shape->num_blocks * shape->num_kv_heads * kBlock * shape->head_dim;
+  a.kv_layer_stride = shape->layer_stride_kv != 0 ? shape->layer_stride_kv
+                                                  : shape->num_blocks * shape->num_kv_heads * kBlock * shape->head_dim;
   a.L = shape->num_layers;
   a.B = shape->batch;
   a.Hkv = shape->num_kv_heads;

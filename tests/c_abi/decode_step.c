@@ -118,6 +118,7 @@ int main(int argc, char** argv) {
   shape.max_seq_len = max_len;
   shape.num_blocks = NB;
   shape.split_blocks = 0;
+  shape.layer_stride_kv = 0;
 
   oda_attn_inputs in;
   memset(&in, 0, sizeof(in));

@@ -49,7 +49,8 @@ def test_param_count_matches_paper(L):
     (dict(num_layers=0), -2), (dict(batch=0), -2), (dict(num_q_heads=7), -2), (dict(head_dim=96), -3),
     (dict(num_q_heads=2 * 17, num_kv_heads=2), -3), (dict(block_size=32), -3), (dict(max_seq_len=0), -2),
     (dict(max_blocks_per_seq=3), -2), (dict(num_blocks=0), -2), (dict(split_blocks=3), -2),
-    (dict(split_blocks=-2), -2)])
+    (dict(split_blocks=-2), -2), (dict(layer_stride_kv=20 * 2 * 16 * 128 - 8), -2),
+    (dict(layer_stride_kv=20 * 2 * 16 * 128 + 4), -2)])
 def test_bad_shapes(L, kw, status):
     with pytest.raises(L.OdaError) as e:
         L.attn_workspace_size(_shape(L, **kw), 4, 16)

@@ -311,3 +311,35 @@ def test_selection_sizes_on_one_workspace(cur):
                     assert np.max(np.abs(ls[:, b] - ref[1][:, b])) <= LSE_ABS
             for b in set(range(12)) - set(rows):
                 assert np.all(o[:, b] == -7.0) and np.all(ls[:, b] == -7.0)
+
+
+@pytest.mark.parametrize("cur", [False, True])
+def test_layer_stride_between_layers(cur):
+    """layer_stride_kv: each layer's blocks start `stride` elements after the
+    previous layer's (here the dense size plus padding, as in one allocation
+    holding several layer groups).  Local and Full read the right layers and
+    match the oracle on the dense copies."""
+    pb = AttnProblem(57, 3, 4, 16, 4, 128, [70, 300, 1, 515], cur=cur, split_blocks=2)
+    P = pb.P
+    dense = pb.nb * pb.Hkv * 16 * pb.D
+    stride = dense + 8 * 37
+    k_pad = torch.zeros(pb.L * stride, dtype=torch.int16, device="cuda")
+    v_pad = torch.zeros(pb.L * stride, dtype=torch.int16, device="cuda")
+    for l in range(pb.L):
+        k_pad[l * stride:l * stride + dense] = pb.dk[l].reshape(-1)
+        v_pad[l * stride:l * stride + dense] = pb.dv[l].reshape(-1)
+    shape = P.Shape(pb.L, pb.B, pb.Hq, pb.Hkv, pb.D, pb.shape.max_blocks_per_seq, pb.shape.max_seq_len, pb.nb,
+                    2, layer_stride_kv=stride)
+    inp = P.inputs(pb.dq, k_pad, v_pad, pb.dtable, pb.dseq, pb.scale, pb.dkc, pb.dvc)
+    for local in (True, False):
+        out, lse = pb.new_out(np.nan)
+        ws = torch.zeros(max(256, P.attn_workspace_size(shape, 4, 64 if local else 0)), dtype=torch.uint8,
+                         device="cuda")
+        if local:
+            P.local_decode_attn(shape, inp, 4, 64, out, lse, ws)
+            want = pb.oracle_local(4, 64)
+        else:
+            P.full_decode_attn(shape, inp, 0, None, None, None, out, lse, ws)
+            want = pb.oracle_full(0)
+        torch.cuda.synchronize()
+        _cmp(pb, (out, lse), want)
