@@ -54,7 +54,7 @@ LLAMA = Workload("llama3-8b", batch=1, num_q_heads=32, num_kv_heads=8, head_dim=
 
 MIXED = Workload("mixed", batch=32, num_q_heads=32, num_kv_heads=8, head_dim=128, stacks=(_gated(32, 2048),),
                  seq_range=(8192, 65536), d_model=4096, d_hidden=256, rhos=(0.1, 0.25, 0.5),
-                 bernoulli=(0.1, 0.25, 0.5), steps=50)
+                 bernoulli=(0.0, 0.1, 0.25, 0.5), steps=50)
 
 LONG = Workload("long", batch=4, num_q_heads=32, num_kv_heads=8, head_dim=128, stacks=(_gated(32, 4096),),
                 seq_lens=(131072,) * 4, d_model=4096, d_hidden=256, rhos=(0.0, 0.05, 0.2, 1.0), steps=100)
