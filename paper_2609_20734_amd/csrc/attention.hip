@@ -782,8 +782,10 @@ void make_plan(const oda_attn_shape* s, int n_sink, int window, int64_t selected
   p->dyn = 0;
   if (bps == 0) {
     const int64_t want = oda::ceil_div(kTargetGroups, units_selected);
-    // at least one block pair per wavefront
-    const int64_t max_split = std::max<int64_t>(1, nvb / (2 * kWaves));
+    // at least kWaves blocks (four block pairs) per split: a small call gets
+    // more, shorter splits, which shortens the split phase more than the merge
+    // of more partials costs (half of a split's wavefronts may be idle)
+    const int64_t max_split = std::max<int64_t>(1, nvb / kWaves);
     const int64_t nsplit = std::max<int64_t>(1, std::min(want, max_split));
     bps = oda::round_up(oda::ceil_div(nvb, nsplit), 2);
     p->dyn = 1;
