@@ -241,6 +241,41 @@ oda_status oda_full_decode_attn(const oda_attn_shape *shape, const oda_attn_inpu
                                 float *lse, void *workspace, size_t workspace_bytes,
                                 hipStream_t stream);
 
+/* Current-token preparation fused into a one-layer attention call (host
+ * struct holding device pointers), for the decoder around the path (below):
+ * the call builds the query and the current candidate K/V itself from the
+ * fp32 QKV projection output, exactly as oda_qk_norm_rope would (per-head
+ * RMSNorm of q and k, rotary embedding at position seq_lens[b] - 1, bf16
+ * rounding; the same device code), instead of reading q / k_cur / v_cur, and
+ * saves that launch.  Results are bit-identical to oda_qk_norm_rope followed
+ * by the plain call.
+ *   qkv     fp32 [B][(Hq + 2 Hkv) D]: q heads, then k heads, then v heads
+ *   q_gain, k_gain  fp32 [D] per-head RMSNorm gains, or NULL (no norm)
+ *   k_out, v_out    bf16 [B][Hkv][D]: the candidate K/V of the requests the
+ *                   call attends (for the commit), or both NULL */
+typedef struct {
+  const float *qkv;
+  const float *q_gain;
+  const float *k_gain;
+  float rms_eps;                /* >= 0                                          */
+  double rope_theta;            /* > 1                                           */
+  uint16_t *k_out;
+  uint16_t *v_out;
+} oda_qkv_prep;
+
+/* oda_local_decode_attn / oda_full_decode_attn of one layer (num_layers == 1)
+ * with the current token prepared in the call (oda_qkv_prep): in->q, k_cur and
+ * v_cur must be NULL; the cache holds positions 0..n_b-2 and position n_b-1 is
+ * the prepared candidate.  Everything else (sets, selection, workspace, the
+ * rows written) is as in the plain calls. */
+oda_status oda_local_decode_attn_qkv(const oda_attn_shape *shape, const oda_attn_inputs *in,
+                                     const oda_qkv_prep *prep, int32_t n_sink, int32_t window, float *out,
+                                     float *lse, void *workspace, size_t workspace_bytes, hipStream_t stream);
+oda_status oda_full_decode_attn_qkv(const oda_attn_shape *shape, const oda_attn_inputs *in,
+                                    const oda_qkv_prep *prep, int32_t native_window, const int32_t *flags,
+                                    const int32_t *work_list, const int32_t *n_work, float *out, float *lse,
+                                    void *workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Bytes of workspace oda_commit_kv needs when it advances the lengths: one
  * ticket word per request, rounded up to 256 bytes (host out).  Zero-fill it
  * before its first use; every call leaves it zero again. */
@@ -278,6 +313,7 @@ oda_status oda_commit_kv(const oda_attn_shape *shape, uint16_t *k_cache, uint16_
  *   q, k, v = split(qkv); q, k per-head RMSNorm and rotary embedding at the
  *   current position, cast to bf16       oda_qk_norm_rope
  *   a = attention(q, cache, k, v)         oda_local_decode_attn / oda_full_decode_attn
+ *   (the last two in one launch: oda_local_decode_attn_qkv / oda_full_decode_attn_qkv)
  *   h = h + W_o . a                       oda_dense_bf16 (residual = h)
  *   m = SiLU(W_g . RMSNorm(h)) * (W_u . RMSNorm(h))   oda_dense_bf16 (SWIGLU)
  *   h = h + W_d . m                       oda_dense_bf16 (residual = h)

@@ -20,7 +20,7 @@ _EXPORTS = ("HEAD_MLP", "HEAD_PAPER", "OdaError", "Shape", "attn_workspace_size"
             "DENSE_PLAIN", "DENSE_SWIGLU", "dense_desc", "dense_bf16", "qk_norm_rope", "embed_bf16", "copy_rows",
             "argmax", "prepare_dense", "prepare_qk_norm_rope", "prepare_embed", "prepare_copy_rows",
             "prepare_argmax", "stream_read", "prepare_stream_read", "rms_norm_rows", "prepare_rms_norm_rows",
-            "recall_gate_static")
+            "recall_gate_static", "qkv_prep", "prepare_local_qkv", "prepare_full_qkv")
 
 
 def __getattr__(name):

@@ -33,6 +33,7 @@ DENSE_PLAIN = 0
 DENSE_SWIGLU = 1
 
 EXPORTED = ("oda_attn_workspace_size", "oda_local_decode_attn", "oda_full_decode_attn",
+            "oda_local_decode_attn_qkv", "oda_full_decode_attn_qkv",
             "oda_gate_param_count", "oda_gate_workspace_size", "oda_recall_gate", "oda_recall_gate_static",
             "oda_commit_workspace_size", "oda_commit_kv",
             "oda_dense_bf16", "oda_qk_norm_rope", "oda_embed_bf16", "oda_copy_rows", "oda_rms_norm_rows",
@@ -61,6 +62,12 @@ class AttnInputs(ctypes.Structure):
                 ("k_cur", ctypes.c_void_p), ("v_cur", ctypes.c_void_p), ("scale", ctypes.c_float)]
 
 
+class QkvPrep(ctypes.Structure):
+    _fields_ = [("qkv", ctypes.c_void_p), ("q_gain", ctypes.c_void_p), ("k_gain", ctypes.c_void_p),
+                ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_double), ("k_out", ctypes.c_void_p),
+                ("v_out", ctypes.c_void_p)]
+
+
 class GateDesc(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("d_model", ctypes.c_int32), ("d_hidden", ctypes.c_int32),
                 ("rms_eps", ctypes.c_float), ("params", ctypes.c_void_p)]
@@ -83,6 +90,14 @@ _lib.oda_full_decode_attn.argtypes = [_P(AttnShape), _P(AttnInputs), ctypes.c_in
                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                       ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
 _lib.oda_full_decode_attn.restype = ctypes.c_int
+_lib.oda_local_decode_attn_qkv.argtypes = [_P(AttnShape), _P(AttnInputs), _P(QkvPrep), ctypes.c_int32,
+                                           ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                           ctypes.c_size_t, ctypes.c_void_p]
+_lib.oda_local_decode_attn_qkv.restype = ctypes.c_int
+_lib.oda_full_decode_attn_qkv.argtypes = [_P(AttnShape), _P(AttnInputs), _P(QkvPrep), ctypes.c_int32,
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+_lib.oda_full_decode_attn_qkv.restype = ctypes.c_int
 _lib.oda_gate_param_count.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P(ctypes.c_int64)]
 _lib.oda_gate_param_count.restype = ctypes.c_int
 _lib.oda_gate_workspace_size.argtypes = [_P(GateDesc), ctypes.c_int32, _P(ctypes.c_size_t)]
@@ -337,6 +352,30 @@ def prepare_local(shape: Shape, inp: AttnInputs, n_sink: int, window: int, out, 
     args = (ctypes.byref(cs), ctypes.byref(inp), n_sink, window, _ptr(out), _ptr(lse), _ptr(workspace),
             _nbytes(workspace, workspace_bytes), _stream(stream))
     return Call(_lib.oda_local_decode_attn, args, (cs, inp, out, lse, workspace))
+
+
+def qkv_prep(qkv, q_gain, k_gain, rms_eps: float, rope_theta: float, k_out=None, v_out=None) -> QkvPrep:
+    """The C struct of a fused call's current-token preparation; it keeps the tensors alive."""
+    s = QkvPrep(_ptr(qkv), _ptr(q_gain), _ptr(k_gain), float(rms_eps), float(rope_theta), _ptr(k_out), _ptr(v_out))
+    s._keep = (qkv, q_gain, k_gain, k_out, v_out)
+    return s
+
+
+def prepare_local_qkv(shape: Shape, inp: AttnInputs, prep: QkvPrep, n_sink: int, window: int, out, lse, workspace,
+                      workspace_bytes: int | None = None, stream=None) -> Call:
+    cs = shape.c()
+    args = (ctypes.byref(cs), ctypes.byref(inp), ctypes.byref(prep), n_sink, window, _ptr(out), _ptr(lse),
+            _ptr(workspace), _nbytes(workspace, workspace_bytes), _stream(stream))
+    return Call(_lib.oda_local_decode_attn_qkv, args, (cs, inp, prep, out, lse, workspace))
+
+
+def prepare_full_qkv(shape: Shape, inp: AttnInputs, prep: QkvPrep, native_window: int, flags, work_list, n_work,
+                     out, lse, workspace, workspace_bytes: int | None = None, stream=None) -> Call:
+    cs = shape.c()
+    args = (ctypes.byref(cs), ctypes.byref(inp), ctypes.byref(prep), native_window, _ptr(flags), _ptr(work_list),
+            _ptr(n_work), _ptr(out), _ptr(lse), _ptr(workspace), _nbytes(workspace, workspace_bytes),
+            _stream(stream))
+    return Call(_lib.oda_full_decode_attn_qkv, args, (cs, inp, prep, flags, work_list, n_work, out, lse, workspace))
 
 
 def prepare_full(shape: Shape, inp: AttnInputs, native_window: int, flags, work_list, n_work, out, lse,

@@ -39,6 +39,7 @@
 #include <cmath>
 
 #include "oda.h"
+#include "oda_device.h"
 #include "oda_internal.h"
 
 namespace {
@@ -90,7 +91,34 @@ struct AttnArgs {
   // to address memory; the affected outputs become NaN (or are skipped)
   int32_t max_len;
   int64_t num_blocks;
+  // fused current-token preparation (the *_qkv entry points, one layer): q
+  // and the candidate K/V are built from the fp32 QKV projection output
+  // instead of being read from q / k_cur / v_cur
+  const float* qkv;      // [B][(Hq + 2 Hkv) D], or NULL (not fused)
+  const float* q_gain;   // [D] or NULL
+  const float* k_gain;   // [D] or NULL
+  uint16_t* k_out;       // [B][Hkv][D]: the candidate K (bf16) for the commit, or NULL
+  uint16_t* v_out;       // [B][Hkv][D]
+  double rope_theta;
+  float rms_eps;
 };
+
+// Where a unit's query rows and current candidate come from: global memory,
+// or the bf16 copy a fused call builds in shared memory.
+struct CurSrc {
+  const uint16_t* q;    // [G][D] rows of the unit's query heads
+  const uint16_t* k;    // [D] candidate K (has_cur only)
+  const uint16_t* v;    // [D] candidate V (has_cur only)
+};
+
+__device__ __forceinline__ CurSrc global_cur(const AttnArgs& a, int D, int l, int b, int g) {
+  CurSrc c;
+  c.q = a.q + (((int64_t)l * a.B + b) * a.Hq + (int64_t)g * a.G) * D;
+  const int64_t coff = (((int64_t)l * a.B + b) * a.Hkv + g) * D;
+  c.k = a.has_cur ? a.k_cur + coff : nullptr;
+  c.v = a.has_cur ? a.v_cur + coff : nullptr;
+  return c;
+}
 
 // Positions of one request attended through the cache, as block ranges.
 //   A = [0, a_end)          the sink part
@@ -373,6 +401,8 @@ __device__ __forceinline__ void consume_pair(PairTile<D>& t, const Run& r, int v
 __host__ __device__ constexpr size_t split_lds_floats(int G, int D) {
   return (size_t)kWaves * 32 + (size_t)kWaves * G * D + 16;
 }
+// A fused call's bf16 query rows and candidate K/V, after the floats above.
+__host__ __device__ constexpr size_t prep_lds_bytes(int G, int D) { return (size_t)(G + 2) * D * 2; }
 
 // Running state of one output element of the split merge: maximum logit M
 // (log2 units), weighted sum of partial outputs and of partial denominators.
@@ -415,7 +445,7 @@ __device__ __forceinline__ void merge_chunk(MergeAcc& m, const float* ml, const 
 // split order, so the result does not depend on which workgroup merges.
 template <int D>
 __device__ __forceinline__ void merge_unit(const AttnArgs& a, int l, int b, int g, int nsplit, float* sm_zc,
-                                           int nthreads) {
+                                           int nthreads, const CurSrc& cur) {
   const int G = a.G;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -423,17 +453,16 @@ __device__ __forceinline__ void merge_unit(const AttnArgs& a, int l, int b, int 
   const float* ml = a.part_ml + pbase * G * 2;
   const float* po = a.part_o + pbase * G * D;
   const int64_t qoff = (((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G) * D;
-  const int64_t coff = (((int64_t)l * a.B + b) * a.Hkv + g) * D;
 
   if (a.has_cur) {
     constexpr int PD = D / 64;
     float kc[PD];
 #pragma unroll
-    for (int e = 0; e < PD; ++e) kc[e] = bf16_to_float(a.k_cur[coff + lane * PD + e]);
+    for (int e = 0; e < PD; ++e) kc[e] = bf16_to_float(cur.k[lane * PD + e]);
     for (int hh = wave; hh < G; hh += nthreads / 64) {
       float dot = 0.f;
 #pragma unroll
-      for (int e = 0; e < PD; ++e) dot += bf16_to_float(a.q[qoff + hh * D + lane * PD + e]) * kc[e];
+      for (int e = 0; e < PD; ++e) dot += bf16_to_float(cur.q[hh * D + lane * PD + e]) * kc[e];
       dot = wave_sum(dot) * a.scale_log2;
       if (lane == 0) sm_zc[hh] = dot;
     }
@@ -448,7 +477,7 @@ __device__ __forceinline__ void merge_unit(const AttnArgs& a, int l, int b, int 
     MergeAcc m;
     if (a.has_cur) {   // the candidate's weight is exp2(zc - M) = 1 at M = zc
       m.M = sm_zc[hh];
-      m.acc = bf16_to_float(a.v_cur[coff + d]);
+      m.acc = bf16_to_float(cur.v[d]);
       m.lam = 1.f;
     }
     for (int s0 = 0; s0 < nsplit;) {
@@ -466,13 +495,50 @@ __device__ __forceinline__ void merge_unit(const AttnArgs& a, int l, int b, int 
   }
 }
 
+// Fused calls: the unit's G query heads, its K head and its V head of the
+// current token, from the fp32 QKV projection output (q heads, then k heads,
+// then v heads per request), one head per wavefront: q and k through the
+// per-head RMSNorm and the rotary embedding at position n - 1 (the shared
+// oda::norm_rope_pair, the same code oda_qk_norm_rope runs), v unchanged,
+// all rounded to bf16 into prep = [G][D] query rows, then K, then V.  The
+// fp32 loads do not depend on n; the rotation does.
+template <int D>
+__device__ __forceinline__ void prepare_current(const AttnArgs& a, int b, int g, int n, uint16_t* prep,
+                                                bool write_out) {
+  constexpr int half = D / 2;
+  const int G = a.G;
+  const int lane = threadIdx.x & 63;
+  const int wave = uniform(threadIdx.x >> 6);
+  const int heads = a.Hq + 2 * a.Hkv;
+  for (int t = wave; t < G + 2; t += kWaves) {   // t < G: query head g G + t; G: K; G + 1: V
+    const int h = t < G ? g * G + t : (t == G ? a.Hq + g : a.Hq + a.Hkv + g);
+    const float* src = a.qkv + ((int64_t)b * heads + h) * D;
+    float x1 = lane < half ? src[lane] : 0.f;
+    float x2 = lane < half ? src[lane + half] : 0.f;
+    if (t <= G)
+      oda::norm_rope_pair(x1, x2, lane < half, lane, D, t < G ? a.q_gain : a.k_gain, a.rms_eps, (double)(n - 1),
+                          a.rope_theta);
+    if (lane < half) {
+      const uint16_t y1 = oda::bf16_rne(x1), y2 = oda::bf16_rne(x2);
+      uint16_t* dst = prep + (int64_t)t * D;
+      dst[lane] = y1;
+      dst[lane + half] = y2;
+      if (write_out && t >= G && a.k_out != nullptr) {
+        uint16_t* o = (t == G ? a.k_out : a.v_out) + ((int64_t)b * a.Hkv + g) * D;
+        o[lane] = y1;
+        o[lane + half] = y2;
+      }
+    }
+  }
+}
+
 // One unit of work: the wavefront runs of r (this split of request b) for
 // layer l and KV head g are streamed, combined across the wavefronts in
 // shared memory and written out (finalised when the request has one split,
 // else as this split's partial).
 template <int D, bool kLocal>
 __device__ __forceinline__ void run_unit(const AttnArgs& a, Run& r, int l, int b, int g, int split, int nsplit,
-                                         float* smem) {
+                                         float* smem, const CurSrc& cur) {
   constexpr int KK = D / 32;   // MFMA k-steps for q.k
   constexpr int NT = D / 16;   // 16-dim output tiles
   const int lane = threadIdx.x & 63;
@@ -496,7 +562,7 @@ __device__ __forceinline__ void run_unit(const AttnArgs& a, Run& r, int l, int b
   if (r.v_lo < r.v_hi) {
     // Q^T as the B operand: column = query head h16 of this KV head's group.
     bf16x8 qf[KK];
-    const uint16_t* qrow = a.q + (((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G + h16) * D;
+    const uint16_t* qrow = cur.q + (int64_t)h16 * D;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) qf[kk] = (h16 < G) ? load16(qrow + 32 * kk + 8 * j) : bf16x8{};
 
@@ -540,17 +606,16 @@ __device__ __forceinline__ void run_unit(const AttnArgs& a, Run& r, int l, int b
   }
   const bool finalize = (nsplit == 1);
   const int64_t qoff = (((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G) * D;
-  const int64_t coff = (((int64_t)l * a.B + b) * a.Hkv + g) * D;
   if (finalize && a.has_cur && wave == 0) {
     // candidate logits of the G heads (log2 units)
     constexpr int PD = D / 64;
     float kc[PD];
 #pragma unroll
-    for (int e = 0; e < PD; ++e) kc[e] = bf16_to_float(a.k_cur[coff + lane * PD + e]);
+    for (int e = 0; e < PD; ++e) kc[e] = bf16_to_float(cur.k[lane * PD + e]);
     for (int hh = 0; hh < G; ++hh) {
       float dot = 0.f;
 #pragma unroll
-      for (int e = 0; e < PD; ++e) dot += bf16_to_float(a.q[qoff + hh * D + lane * PD + e]) * kc[e];
+      for (int e = 0; e < PD; ++e) dot += bf16_to_float(cur.q[hh * D + lane * PD + e]) * kc[e];
       dot = wave_sum(dot) * a.scale_log2;
       if (lane == 0) sm_zc[hh] = dot;
     }
@@ -576,7 +641,7 @@ __device__ __forceinline__ void run_unit(const AttnArgs& a, Run& r, int l, int b
         const float z = sm_zc[hh];
         const float M2 = fmaxf(M, z);
         const float s_old = exp2_fast(M - M2), s_cur = exp2_fast(z - M2);
-        acc = acc * s_old + s_cur * bf16_to_float(a.v_cur[coff + d]);
+        acc = acc * s_old + s_cur * bf16_to_float(cur.v[d]);
         lam = lam * s_old + s_cur;
         M = M2;
       }
@@ -620,6 +685,20 @@ void attn_split_kernel(AttnArgs a) {
   b = uniform(b);
   const int n = uniform(a.seq_lens[b]);
   const int G = a.G;
+  CurSrc cur;
+  if (a.qkv != nullptr) {
+    // fused call: this workgroup builds the unit's bf16 query rows and the
+    // candidate K/V in shared memory (every split the same values); split 0
+    // also writes the candidate out for the commit
+    uint16_t* prep = reinterpret_cast<uint16_t*>(smem + split_lds_floats(G, D));
+    prepare_current<D>(a, b, g, n, prep, split == 0);
+    __syncthreads();
+    cur.q = prep;
+    cur.k = prep + G * D;
+    cur.v = prep + (G + 1) * D;
+  } else {
+    cur = global_cur(a, D, l, b, g);
+  }
   if (!valid_len(a, n)) {   // no history is addressed: the request's rows become NaN
     if (split == 0) {
       const int64_t q0 = (((int64_t)l * a.B + b) * a.Hq + (int64_t)g * G) * D;
@@ -645,7 +724,7 @@ void attn_split_kernel(AttnArgs a) {
   r.v_lo = min(v_end, v_begin + 2 * per_wave * wave);
   r.v_hi = min(v_end, r.v_lo + 2 * per_wave);
 
-  run_unit<D, kLocal>(a, r, l, b, g, split, nsplit, smem);
+  run_unit<D, kLocal>(a, r, l, b, g, split, nsplit, smem, cur);
   if (nsplit == 1) return;   // finalised
   float* sm_zc = smem + kWaves * 32 + kWaves * G * D;
   // The last of the request's splits to finish merges them all.  The eight
@@ -670,7 +749,7 @@ void attn_split_kernel(AttnArgs a) {
   __syncthreads();
   if (!last_split) return;
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  merge_unit<D>(a, l, b, g, nsplit, sm_zc, kWaves * 64);
+  merge_unit<D>(a, l, b, g, nsplit, sm_zc, kWaves * 64, cur);
 }
 
 // Batched Local with one split per unit and many units per CU: a work item is
@@ -712,7 +791,7 @@ void attn_local_layers_kernel(AttnArgs a) {
   r.v_lo = min(r.geo.nvb, 2 * per_wave * wave);
   r.v_hi = min(r.geo.nvb, r.v_lo + 2 * per_wave);
   for (int l = l0; l < l1; ++l) {
-    run_unit<D, true>(a, r, l, b, g, 0, 1, smem);
+    run_unit<D, true>(a, r, l, b, g, 0, 1, smem, global_cur(a, D, l, b, g));
     __syncthreads();   // the next layer reuses the shared memory
   }
 }
@@ -811,13 +890,29 @@ void make_plan(const oda_attn_shape* s, int n_sink, int window, int64_t selected
   p->bytes = (size_t)(t_bytes + o_bytes + ml_bytes);
 }
 
-oda_status check_inputs(const oda_attn_inputs* in, const float* out) {
+oda_status check_inputs(const oda_attn_inputs* in, const float* out, const oda_attn_shape* s = nullptr,
+                        const oda_qkv_prep* prep = nullptr) {
   if (in == nullptr) return oda::fail(ODA_ERR_NULL, "inputs is NULL");
-  if (!in->q || !in->k_cache || !in->v_cache || !in->block_table || !in->seq_lens || !out)
-    return oda::fail(ODA_ERR_NULL, "q, k_cache, v_cache, block_table, seq_lens and out are required");
+  if (prep != nullptr) {   // fused current-token preparation: q and the candidate come from prep
+    if (in->q || in->k_cur || in->v_cur)
+      return oda::fail(ODA_ERR_SHAPE, "with oda_qkv_prep, q, k_cur and v_cur must be NULL");
+    if (!prep->qkv) return oda::fail(ODA_ERR_NULL, "prep->qkv is required");
+    if ((prep->k_out == nullptr) != (prep->v_out == nullptr))
+      return oda::fail(ODA_ERR_NULL, "prep->k_out and prep->v_out must both be NULL or both be set");
+    if (s->num_layers != 1) return oda::fail(ODA_ERR_SHAPE, "a call with oda_qkv_prep has one layer (got %d)",
+                                             s->num_layers);
+    if (!(prep->rope_theta > 1.0) || !std::isfinite(prep->rope_theta))
+      return oda::fail(ODA_ERR_SHAPE, "prep->rope_theta must be > 1");
+    if (!(prep->rms_eps >= 0.f) || !std::isfinite(prep->rms_eps))
+      return oda::fail(ODA_ERR_SHAPE, "prep->rms_eps must be >= 0");
+  } else if (!in->q) {
+    return oda::fail(ODA_ERR_NULL, "q is required");
+  }
+  if (!in->k_cache || !in->v_cache || !in->block_table || !in->seq_lens || !out)
+    return oda::fail(ODA_ERR_NULL, "k_cache, v_cache, block_table, seq_lens and out are required");
   if ((in->k_cur == nullptr) != (in->v_cur == nullptr))
     return oda::fail(ODA_ERR_NULL, "k_cur and v_cur must both be NULL or both be set");
-  if (!oda::aligned(in->q, 16) || !oda::aligned(in->k_cache, 16) || !oda::aligned(in->v_cache, 16) ||
+  if ((in->q && !oda::aligned(in->q, 16)) || !oda::aligned(in->k_cache, 16) || !oda::aligned(in->v_cache, 16) ||
       !oda::aligned(out, 16) || (in->k_cur && (!oda::aligned(in->k_cur, 16) || !oda::aligned(in->v_cur, 16))))
     return oda::fail(ODA_ERR_SHAPE, "q, caches, k_cur, v_cur and out must be 16-byte aligned");
   if (!(in->scale > 0.f) || !std::isfinite(in->scale))
@@ -871,10 +966,10 @@ oda_status launch(const AttnArgs& args, const Plan& plan, hipStream_t stream) {
   const int64_t units = (int64_t)args.L * args.B * args.Hkv;
   const int64_t items = units * plan.max_splits;
   if (items > 0x7fffffffLL) return oda::fail(ODA_ERR_SHAPE, "grid too large (%lld work items)", (long long)items);
-  const size_t lds = split_lds_floats(args.G, D) * sizeof(float);
+  const size_t lds = split_lds_floats(args.G, D) * sizeof(float) + (args.qkv ? prep_lds_bytes(args.G, D) : 0);
   static std::atomic<uint64_t> lds_raised{0};
   raise_lds_limit(reinterpret_cast<const void*>(attn_split_kernel<D, kLocal>), &lds_raised,
-                  (int)(split_lds_floats(kMaxGroup, D) * 4));
+                  (int)(split_lds_floats(kMaxGroup, D) * 4 + prep_lds_bytes(kMaxGroup, D)));
   (void)hipGetLastError();
   hipLaunchKernelGGL((attn_split_kernel<D, kLocal>), dim3((unsigned)items), dim3(kWaves * 64), lds, stream, args);
   const hipError_t e = hipGetLastError();
@@ -884,7 +979,8 @@ oda_status launch(const AttnArgs& args, const Plan& plan, hipStream_t stream) {
 
 oda_status run_attention(const oda_attn_shape* s, const oda_attn_inputs* in, bool local, int n_sink, int window,
                          int select, const int32_t* flags, const int32_t* work_list, const int32_t* n_work,
-                         float* out, float* lse, void* ws, size_t ws_bytes, hipStream_t stream) {
+                         float* out, float* lse, void* ws, size_t ws_bytes, hipStream_t stream,
+                         const oda_qkv_prep* prep = nullptr) {
   Plan plan;
   // Local attends every request; Full is sized for the fewest selected (one)
   make_plan(s, n_sink, window, local ? s->batch : 1, &plan);
@@ -921,7 +1017,14 @@ oda_status run_attention(const oda_attn_shape* s, const oda_attn_inputs* in, boo
   a.MB = s->max_blocks_per_seq;
   a.n_sink = n_sink;
   a.window = window;
-  a.has_cur = in->k_cur != nullptr;
+  a.has_cur = (in->k_cur != nullptr || prep != nullptr) ? 1 : 0;
+  a.qkv = prep ? prep->qkv : nullptr;
+  a.q_gain = prep ? prep->q_gain : nullptr;
+  a.k_gain = prep ? prep->k_gain : nullptr;
+  a.k_out = prep ? prep->k_out : nullptr;
+  a.v_out = prep ? prep->v_out : nullptr;
+  a.rope_theta = prep ? prep->rope_theta : 0.0;
+  a.rms_eps = prep ? prep->rms_eps : 0.f;
   a.bps = plan.bps;
   a.max_splits = plan.max_splits;
   a.dyn_splits = plan.dyn;
@@ -963,6 +1066,39 @@ extern "C" oda_status oda_local_decode_attn(const oda_attn_shape* shape, const o
   if (window < 1) return oda::fail(ODA_ERR_SHAPE, "window must be >= 1 for Local attention");
   return run_attention(shape, in, true, n_sink, window, kSelAll, nullptr, nullptr, nullptr, out, lse, workspace,
                        workspace_bytes, stream);
+}
+
+extern "C" oda_status oda_local_decode_attn_qkv(const oda_attn_shape* shape, const oda_attn_inputs* in,
+                                               const oda_qkv_prep* prep, int32_t n_sink, int32_t window, float* out,
+                                               float* lse, void* workspace, size_t workspace_bytes,
+                                               hipStream_t stream) {
+  oda_status st = check_shape(shape);
+  if (st != ODA_OK) return st;
+  if (prep == nullptr) return oda::fail(ODA_ERR_NULL, "prep is NULL");
+  st = check_inputs(in, out, shape, prep);
+  if (st != ODA_OK) return st;
+  if (n_sink < 0) return oda::fail(ODA_ERR_SHAPE, "n_sink must be >= 0");
+  if (window < 1) return oda::fail(ODA_ERR_SHAPE, "window must be >= 1 for Local attention");
+  return run_attention(shape, in, true, n_sink, window, kSelAll, nullptr, nullptr, nullptr, out, lse, workspace,
+                       workspace_bytes, stream, prep);
+}
+
+extern "C" oda_status oda_full_decode_attn_qkv(const oda_attn_shape* shape, const oda_attn_inputs* in,
+                                              const oda_qkv_prep* prep, int32_t native_window,
+                                              const int32_t* flags, const int32_t* work_list,
+                                              const int32_t* n_work, float* out, float* lse, void* workspace,
+                                              size_t workspace_bytes, hipStream_t stream) {
+  oda_status st = check_shape(shape);
+  if (st != ODA_OK) return st;
+  if (prep == nullptr) return oda::fail(ODA_ERR_NULL, "prep is NULL");
+  st = check_inputs(in, out, shape, prep);
+  if (st != ODA_OK) return st;
+  if (native_window < 0) return oda::fail(ODA_ERR_SHAPE, "native_window must be >= 0");
+  if ((work_list == nullptr) != (n_work == nullptr))
+    return oda::fail(ODA_ERR_NULL, "work_list and n_work must both be NULL or both be set");
+  const int select = work_list ? kSelList : (flags ? kSelFlags : kSelAll);
+  return run_attention(shape, in, false, 0, native_window, select, flags, work_list, n_work, out, lse, workspace,
+                       workspace_bytes, stream, prep);
 }
 
 extern "C" oda_status oda_full_decode_attn(const oda_attn_shape* shape, const oda_attn_inputs* in,

@@ -26,6 +26,7 @@
 #include <cmath>
 
 #include "oda.h"
+#include "oda_device.h"
 #include "oda_internal.h"
 
 namespace {
@@ -39,11 +40,7 @@ constexpr int kDenseMinWaves = 2048;   // grouping rows stops short of fewer wav
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-__device__ __forceinline__ uint16_t to_bf16(float f) {   // round to nearest, ties to even
-  const uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
-  return (uint16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
-}
+__device__ __forceinline__ uint16_t to_bf16(float f) { return oda::bf16_rne(f); }
 __device__ __forceinline__ float silu(float x) { return x / (1.f + __expf(-x)); }
 __device__ __forceinline__ float wave_sum(float x) {
 #pragma unroll
@@ -225,9 +222,9 @@ struct RopeArgs {
   int B, Hq, Hkv, D, heads_per_group;
 };
 
-// One wavefront per (selected request, head).  Lane i < D/2 holds the pair
-// (x_i, x_{i+D/2}) that the rotation mixes (rotate-half convention); angles
-// are formed in double precision, since positions reach 10^5-10^6.
+// One wavefront per (selected request, head); q and k heads go through
+// oda::norm_rope_pair (the same code the fused attention calls run), v heads
+// are only rounded.
 __global__ __launch_bounds__(256) void qk_norm_rope_kernel(RopeArgs p) {
   const int lane = threadIdx.x & 63;
   const int wave = uniform(threadIdx.x >> 6);
@@ -244,27 +241,9 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(RopeArgs p) {
   uint16_t* dst;
   if (h < p.Hq + p.Hkv) {
     const bool is_q = h < p.Hq;
-    const float* gain = is_q ? p.q_gain : p.k_gain;
-    if (gain != nullptr) {
-      // every lane takes part in the sum (the inactive ones add zeros), so it
-      // is whole for any D / 2 up to 64, not only powers of two
-      float ss = x1 * x1 + x2 * x2;
-#pragma unroll
-      for (int s = 32; s >= 1; s >>= 1) ss += __shfl_xor(ss, s);
-      const float inv = rsqrtf(ss / (float)p.D + p.eps);
-      if (active) {
-        x1 = x1 * inv * gain[lane];
-        x2 = x2 * inv * gain[lane + half];
-      }
-    }
+    oda::norm_rope_pair(x1, x2, active, lane, p.D, is_q ? p.q_gain : p.k_gain, p.eps,
+                        (double)(p.seq_lens[b] - 1), p.theta);
     if (!active) return;
-    const double pos = (double)(p.seq_lens[b] - 1);
-    const double ang = pos * pow(p.theta, -(double)(2 * lane) / (double)p.D);
-    const float c = (float)cos(ang), s = (float)sin(ang);
-    const float r1 = x1 * c - x2 * s;
-    const float r2 = x2 * c + x1 * s;
-    x1 = r1;
-    x2 = r2;
     dst = is_q ? p.q_out + ((int64_t)b * p.Hq + h) * p.D : p.k_out + ((int64_t)b * p.Hkv + (h - p.Hq)) * p.D;
   } else {
     if (!active) return;

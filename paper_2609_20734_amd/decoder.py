@@ -64,17 +64,22 @@ class Decoder:
     (bf16 weights, fp32 gains); cache, table and lengths as the attention ABI
     takes them; gate: a GateDesc for the recall head (None: no gate);
     prescribed: the gate takes its flags from `self.forced` (int32 [B], written
-    before each step) instead of comparing the score with tau (App. B.7)."""
+    before each step) instead of comparing the score with tau (App. B.7);
+    fused_prep: each attention call builds its query and candidate K/V from the
+    QKV projection itself (oda_*_decode_attn_qkv, bit-identical), else
+    oda_qk_norm_rope runs as a launch of its own before it."""
 
     def __init__(self, shape: DecoderShape, weights: dict, batch: int, k_cache, v_cache, block_table, seq_lens,
                  max_blocks_per_seq: int, max_seq_len: int, num_blocks: int, n_sink: int, window: int,
-                 gate=None, tau: float = 0.0, prescribed: bool = False, split_blocks: int = 0):
+                 gate=None, tau: float = 0.0, prescribed: bool = False, split_blocks: int = 0,
+                 fused_prep: bool = True):
         import torch
         s, B = shape, batch
         dev = k_cache.device
         self.shape, self.B, self.w = s, B, weights
         self.k_cache, self.v_cache, self.table, self.seq_lens = k_cache, v_cache, block_table, seq_lens
         self.n_sink, self.window = n_sink, window
+        self.fused_prep = fused_prep
         f32 = dict(dtype=torch.float32, device=dev)
         bf = dict(dtype=torch.bfloat16, device=dev)
         i32 = dict(dtype=torch.int32, device=dev)
@@ -131,16 +136,28 @@ class Decoder:
         calls = []
         for l in range(s.num_layers):
             calls.append(P.prepare_dense(self.d_qkv[l], B, h, None, self.qkv, *wl))
-            calls.append(P.prepare_qk_norm_rope(B, s.num_q_heads, s.num_kv_heads, s.head_dim, self.qkv,
-                                                self.w["q_norm"][l], self.w["k_norm"][l], s.rms_eps, s.rope_theta,
-                                                self.seq_lens, self.q, k_cand[l], v_cand[l], *wl))
-            inp = P.inputs(self.q, self.k_cache[l], self.v_cache[l], self.table, self.seq_lens, self.scale,
-                           k_cand[l], v_cand[l])
-            if branch == "local":
-                calls.append(P.prepare_local(self.attn_shape, inp, self.n_sink, self.window, self.attn, self.lse,
-                                             self.ws_local))
+            if self.fused_prep:
+                prep = P.qkv_prep(self.qkv, self.w["q_norm"][l], self.w["k_norm"][l], s.rms_eps, s.rope_theta,
+                                  k_cand[l], v_cand[l])
+                inp = P.inputs(None, self.k_cache[l], self.v_cache[l], self.table, self.seq_lens, self.scale)
+                if branch == "local":
+                    calls.append(P.prepare_local_qkv(self.attn_shape, inp, prep, self.n_sink, self.window, self.attn,
+                                                     self.lse, self.ws_local))
+                else:
+                    calls.append(P.prepare_full_qkv(self.attn_shape, inp, prep, 0, None, *wl, self.attn, self.lse,
+                                                    self.ws_full))
             else:
-                calls.append(P.prepare_full(self.attn_shape, inp, 0, None, *wl, self.attn, self.lse, self.ws_full))
+                calls.append(P.prepare_qk_norm_rope(B, s.num_q_heads, s.num_kv_heads, s.head_dim, self.qkv,
+                                                    self.w["q_norm"][l], self.w["k_norm"][l], s.rms_eps,
+                                                    s.rope_theta, self.seq_lens, self.q, k_cand[l], v_cand[l], *wl))
+                inp = P.inputs(self.q, self.k_cache[l], self.v_cache[l], self.table, self.seq_lens, self.scale,
+                               k_cand[l], v_cand[l])
+                if branch == "local":
+                    calls.append(P.prepare_local(self.attn_shape, inp, self.n_sink, self.window, self.attn,
+                                                 self.lse, self.ws_local))
+                else:
+                    calls.append(P.prepare_full(self.attn_shape, inp, 0, None, *wl, self.attn, self.lse,
+                                                self.ws_full))
             calls.append(P.prepare_dense(self.d_o[l], B, self.attn, h, h, *wl))
             calls.append(P.prepare_dense(self.d_gu[l], B, h, None, self.mlp, *wl))
             calls.append(P.prepare_dense(self.d_down[l], B, self.mlp, h, h, *wl))

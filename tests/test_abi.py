@@ -110,6 +110,42 @@ def test_full_rejects_bad_arguments(L):
     assert e.value.status == -2
 
 
+def test_fused_prep_calls_reject_bad_arguments(L):
+    """oda_*_decode_attn_qkv: one layer, q / k_cur / v_cur NULL, prep complete and sane."""
+    s1 = _shape(L, num_layers=1)
+    wb = L.attn_workspace_size(s1, 4, 16)
+
+    def prep(**kw):
+        base = dict(qkv=0x3000, q_gain=0x4000, k_gain=0x5000, rms_eps=1e-6, rope_theta=1e6, k_out=0x6000,
+                    v_out=0x7000)
+        base.update(kw)
+        return L.qkv_prep(**base)
+
+    cases = [
+        (s1, dict(q=None), prep(qkv=None), -1),                     # qkv missing
+        (s1, dict(q=None), prep(v_out=None), -1),                   # k_out without v_out
+        (s1, dict(), prep(), -2),                                   # q must be NULL
+        (s1, dict(q=None, k_cur=0x6000, v_cur=0x8000), prep(), -2),  # the candidate comes from prep
+        (_shape(L, num_layers=2), dict(q=None), prep(), -2),        # one layer only
+        (s1, dict(q=None), prep(rope_theta=1.0), -2),
+        (s1, dict(q=None), prep(rope_theta=math.nan), -2),
+        (s1, dict(q=None), prep(rms_eps=-1e-6), -2),
+    ]
+    for shape, kw, pr, status in cases:
+        wbs = L.attn_workspace_size(shape, 4, 16)
+        for call in (L.prepare_local_qkv(shape, _inputs(L, **kw), pr, 4, 16, 0x9000, None, 0x100000, wbs, stream=0),
+                     L.prepare_full_qkv(shape, _inputs(L, **kw), pr, 0, None, None, None, 0x9000, None, 0x100000,
+                                        L.attn_workspace_size(shape, 0, 0), stream=0)):
+            with pytest.raises(L.OdaError) as e:
+                call()
+            assert e.value.status == status, (kw, e.value)
+    # a NULL prep struct
+    cs = s1.c()
+    inp = _inputs(L, q=None)
+    assert L._lib.oda_local_decode_attn_qkv(ctypes.byref(cs), ctypes.byref(inp), None, 4, 16, 0x9000, None,
+                                            0x100000, wb, None) == -1
+
+
 def test_gate_rejects_bad_arguments(L):
     g = L.gate_desc(L.HEAD_PAPER, 64, 16, 0x8000)
     wb = L.gate_workspace_size(g, 4)

@@ -160,7 +160,7 @@ def test_embed_copy_rows_argmax():
 class Tiny:
     """A 2-layer decoder over a paged cache, on the device and in the oracle."""
 
-    def __init__(self, seed=3, B=3, T=4, seq0=(1, 30, 90), s=4, W=24, head="paper"):
+    def __init__(self, seed=3, B=3, T=4, seq0=(1, 30, 90), s=4, W=24, head="paper", fused_prep=True):
         P = self.P = need_gpu()
         from paper_2609_20734_amd import decoder as PD
         L, d, Hq, Hkv, D, F, V = 2, 128, 4, 2, 64, 192, 512
@@ -183,7 +183,8 @@ class Tiny:
         self.dk, self.dv = dev_u16(self.k), dev_u16(self.v)
         self.dtab, self.dseq = dev_i32(self.table), dev_i32(self.seq0)
         self.dec = PD.Decoder(self.shape, dw, B, self.dk, self.dv, self.dtab, self.dseq, self.mb,
-                              int(self.seq0.max()) + T, nb, s, W, gate=self.gate, tau=0.0, prescribed=True)
+                              int(self.seq0.max()) + T, nb, s, W, gate=self.gate, tau=0.0, prescribed=True,
+                              fused_prep=fused_prep)
 
 
 def test_decoder_steps_match_oracle():
@@ -227,6 +228,33 @@ def test_decoder_steps_match_oracle():
     _bf16_close(t.dk.cpu().numpy().view(np.uint16), hk, "K cache")
     _bf16_close(t.dv.cpu().numpy().view(np.uint16), hv, "V cache")
     assert int(dec.counter.item()) == int(forced.sum())
+
+
+def test_fused_preparation_steps_equal_separate_launches():
+    """Whole ODA steps with each attention call preparing its own query and
+    candidate (oda_*_decode_attn_qkv) equal, bit for bit, the same steps with
+    oda_qk_norm_rope as a launch of its own: hidden states, scores, logits,
+    tokens, caches and lengths."""
+    forced = np.array([[1, 0, 1], [0, 0, 0], [1, 1, 1], [0, 1, 0]], dtype=np.int32)
+    results = []
+    for fused in (True, False):
+        t = Tiny(seed=6, fused_prep=fused)
+        dec = t.dec
+        local, retry, out = dec.oda_stages()
+        per_step = []
+        for step in range(t.T):
+            dec.tokens.copy_(torch.from_numpy(t.tokens[step]))
+            dec.forced.copy_(torch.from_numpy(forced[step]))
+            for c in local + retry + out:
+                c()
+            torch.cuda.synchronize()
+            per_step.append([x.clone() for x in (dec.h, dec.h_prev, dec.score, dec.logits, dec.next_token)])
+        results.append((per_step, t.dk.clone(), t.dv.clone(), t.dseq.clone()))
+    (fa, fk, fv, fs), (ua, uk, uv, us) = results
+    for step, (a, b) in enumerate(zip(fa, ua)):
+        for x, y in zip(a, b):
+            assert torch.equal(x, y), step
+    assert torch.equal(fk, uk) and torch.equal(fv, uv) and torch.equal(fs, us)
 
 
 def test_decoder_stage_graphs_replay_bit_exactly():
