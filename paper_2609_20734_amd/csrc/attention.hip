@@ -863,8 +863,12 @@ void make_plan(const oda_attn_shape* s, int n_sink, int window, int64_t selected
     const int64_t want = oda::ceil_div(kTargetGroups, units_selected);
     // at least kWaves blocks (four block pairs) per split: a small call gets
     // more, shorter splits, which shortens the split phase more than the merge
-    // of more partials costs (half of a split's wavefronts may be idle)
-    const int64_t max_split = std::max<int64_t>(1, nvb / kWaves);
+    // of more partials costs (half of a split's wavefronts may be idle).  More
+    // than kMergeChunk splits add a round trip to the merge, so they are taken
+    // only while each split still has 8 * kWaves blocks (four pairs per
+    // wavefront)
+    const int64_t max_split =
+        std::max<int64_t>(1, std::min<int64_t>(nvb / kWaves, std::max<int64_t>(kMergeChunk, nvb / (8 * kWaves))));
     const int64_t nsplit = std::max<int64_t>(1, std::min(want, max_split));
     bps = oda::round_up(oda::ceil_div(nvb, nsplit), 2);
     p->dyn = 1;
