@@ -97,9 +97,10 @@ def _run_both(P, pr, D, Hq, Hkv, branch, s=4, W=64, split_blocks=0, select="all"
 
 
 def _assert_identical(res):
+    """Bit patterns equal (NaN rows of invalid requests included)."""
     (ou, lu, ku, vu), (of, lf, kf, vf) = res
-    assert torch.equal(ou, of), float((ou - of).abs().max())
-    assert torch.equal(lu, lf)
+    assert torch.equal(ou.view(torch.int32), of.view(torch.int32)), float((ou - of).abs().nan_to_num().max())
+    assert torch.equal(lu.view(torch.int32), lf.view(torch.int32))
     assert torch.equal(ku.view(torch.int16), kf.view(torch.int16))
     assert torch.equal(vu.view(torch.int16), vf.view(torch.int16))
 
@@ -141,6 +142,22 @@ def test_native_window_full_fused():
     D, Hq, Hkv = 64, 4, 2
     pr = _problem(P, 9, D, Hq, Hkv, [10, 500], False)
     _assert_identical(_run_both(P, pr, D, Hq, Hkv, "full", native=48))
+
+
+@pytest.mark.parametrize("branch", ["local", "full"])
+def test_invalid_length_gives_nan_rows_both_ways(branch):
+    """A length above max_seq_len addresses no history in either path: that
+    request's rows are NaN, its candidate is still prepared (as
+    oda_qk_norm_rope prepares it), and the other requests are unaffected."""
+    P = need_gpu()
+    D, Hq, Hkv = 64, 8, 2
+    pr = _problem(P, 13, D, Hq, Hkv, [40, 300, 77], True)
+    pr["dseq"][1] = 301                      # above the shape's max_seq_len (300)
+    res = _run_both(P, pr, D, Hq, Hkv, branch, split_blocks=2)
+    _assert_identical(res)
+    out = res[1][0]
+    assert torch.isnan(out[0, 1]).all()
+    assert not torch.isnan(out[0, 0]).any() and not torch.isnan(out[0, 2]).any()
 
 
 def test_fused_local_matches_the_oracle():
