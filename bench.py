@@ -846,6 +846,46 @@ def run_per_layer(b, wl, args, points):
     return base, out
 
 
+def extra_config(name, args):
+    """A shortened run of another workload in the same process: the always-Full
+    step, the threshold (and Bernoulli) sweep of the App. A.2 head with each
+    point's flags checked against the fp64 oracle head, and the roofline
+    launch with its counter traffic.  No warm timing, per-layer mode, decode
+    loop or second head."""
+    import copy
+
+    import torch
+
+    from paper_2609_20734_amd import workloads as WL
+    wl = WL.ALL[name]
+    K = wl.steps
+    oracle = oracle_gate_scores(wl, args.seed, K)
+    b = Bench(wl, "paper", args.seed, K)
+    b.oracle_scores = oracle
+    sub = copy.copy(args)
+    sub.no_warm = True
+    fulls = [b.timed(b.full_calls(), args.warmup if i == 0 else 2, cold=True) for i in range(args.reps)]
+    full_us = float(np.median([f["us_mean"] for f in fulls]))
+    sweep = run_sweep(b, wl, sub, full_us)
+    local_b, gate_b, full_b = bytes_for(wl, b.seq_host, None, "paper")
+    bytes_full = sum(full_b)
+    t = b.kernel_time(b.full_calls()[0], reps=ROOFLINE_REPS, cold=True)
+    ceil_full = b.read_ceiling(bytes_full)
+    roof = dict(bound="hbm", achieved=bytes_full / t / 1e3, peak=HBM_PEAK_GBS, unit="GB/s",
+                traffic=measured_traffic(wl.name, bytes_full), bytes_per_launch=bytes_full, us_per_launch=t,
+                read_ceiling_GBps=ceil_full["GBps"])
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    out = dict(workload=f"{wl.name}: {wl.num_layers} layers, B={wl.batch}, {wl.num_q_heads}q/{wl.num_kv_heads}kv heads, "
+                        f"D={wl.head_dim}, n={'/'.join(str(x) for x in sorted(set(b.seq_host.tolist()))[:4])}, "
+                        f"W={wl.stacks[-1].local_window}, s={wl.stacks[-1].local_sink}, paper recall head "
+                        f"{wl.d_model}->{wl.d_hidden}->1, cold",
+               steps=K, reps=args.reps, always_full_us=round(full_us, 3),
+               sweep=[rounded(e) for e in sweep], roofline=rounded(roof))
+    del b
+    torch.cuda.empty_cache()
+    return out
+
+
 def rounded(d, nd=4):
     return {k: (round(v, nd) if isinstance(v, float) else v) for k, v in d.items()}
 
@@ -1019,6 +1059,8 @@ def main():
                     help="time whole steps of the synthetic decoder (tokens/s) instead of the attention path")
     ap.add_argument("--lengths", default="", help="--decoder: comma-separated context lengths")
     ap.add_argument("--decoder-steps", type=int, default=64, help="--decoder: timed steps per method")
+    ap.add_argument("--extra-configs", default="llama3-8b",
+                    help="comma-separated workloads given a shortened run after the main one ('' for none)")
     ap.add_argument("--roofline-only", action="store_true",
                     help="only the counter legs (Local, empty Full, the roofline Full launch) plus a 1 GiB copy, "
                          "for PMC profiling")
@@ -1164,6 +1206,17 @@ def main():
     }
     if gated_only:
         res["sweep_gated_only"] = [rounded(e) for e in gated_only]
+    extras = [c for c in args.extra_configs.split(",") if c and c != wl.name]
+    if extras:
+        del b
+        torch.cuda.empty_cache()
+        res["extra_configs"] = {}
+        for c in extras:
+            res["extra_configs"][c] = extra_config(c, args)
+            e = res["extra_configs"][c]
+            log(f"[bench] {c}: always-Full {e['always_full_us']:.1f} us/step, roofline "
+                f"{e['roofline']['frac']:.3f} of 8 TB/s; " + ", ".join(
+                    f"rho={p['rho']}: {p['us']:.1f} us x{p['linearity']:.2f}" for p in e["sweep"]))
     if cb is not None:
         cbr = rounded(cb, 3)
         cbr["pool"] = rounded(cb["pool"], 3)
