@@ -846,6 +846,54 @@ def run_per_layer(b, wl, args, points):
     return base, out
 
 
+def gate_only(wl, args):
+    """The recall gate alone, for counter profiling: both heads at the
+    workload's batch and widths, ROOFLINE_REPS cold calls each (App. A.2 head
+    first, then the MLP stand-in), then three 1 GiB copies for the counters'
+    calibration.  Prints one JSON line with the calls' times and algorithmic
+    bytes (fp32 weights + inputs + outputs, the ledger's)."""
+    import torch
+
+    import oda_synth as S
+    import paper_2609_20734_amd as P
+    from paper_2609_20734_amd import ledger as LG
+    dev = torch.device("cuda:0")
+    flush = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    B = wl.batch
+    h, e, l_ = (torch.from_numpy(x[0]).to(dev) for x in S.gate_inputs(args.seed, 1, B, wl.d_model))
+    score = torch.zeros(B, device=dev)
+    flags = torch.zeros(B, dtype=torch.int32, device=dev)
+    work = torch.zeros(B, dtype=torch.int32, device=dev)
+    n_work = torch.zeros(1, dtype=torch.int32, device=dev)
+    out = {}
+    for head in ("paper", "mlp"):
+        kind = P.HEAD_PAPER if head == "paper" else P.HEAD_MLP
+        params = torch.from_numpy(S.gate_params(args.seed, head, wl.d_model, wl.d_hidden)).to(dev)
+        g = P.gate_desc(kind, wl.d_model, wl.d_hidden, params, 1e-6)
+        ws = torch.zeros(P.gate_workspace_size(g, B), dtype=torch.uint8, device=dev)
+        call = P.prepare_gate(g, B, h, e, l_, 0.0, None, score, flags, work, n_work, None, ws)
+        call()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(ROOFLINE_REPS):
+            flush.max()
+            a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            call()
+            b_.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b_) * 1e3)
+        out[head] = dict(us_per_call=float(np.median(ts)), bytes=LG.gate_bytes(head, B, wl.d_model, wl.d_hidden),
+                         calls=1 + ROOFLINE_REPS)
+    src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"gate_only": True, "workload": wl.name, "batch": B, "d_model": wl.d_model,
+                      "d_hidden": wl.d_hidden, "heads": out, "copy_bytes": 1 << 30}), flush=True)
+
+
 def extra_config(name, args):
     """A shortened run of another workload in the same process: the always-Full
     step, the threshold (and Bernoulli) sweep of the App. A.2 head with each
@@ -1061,6 +1109,8 @@ def main():
     ap.add_argument("--decoder-steps", type=int, default=64, help="--decoder: timed steps per method")
     ap.add_argument("--extra-configs", default="llama3-8b",
                     help="comma-separated workloads given a shortened run after the main one ('' for none)")
+    ap.add_argument("--gate-only", action="store_true",
+                    help="only the recall gate (both heads) plus a 1 GiB copy, for PMC profiling")
     ap.add_argument("--roofline-only", action="store_true",
                     help="only the counter legs (Local, empty Full, the roofline Full launch) plus a 1 GiB copy, "
                          "for PMC profiling")
@@ -1076,6 +1126,9 @@ def main():
 
     from paper_2609_20734_amd import workloads as WL
     wl = WL.ALL[args.config]
+    if args.gate_only:
+        gate_only(wl, args)
+        return
     K = args.steps if args.steps > 0 else wl.steps
     args.reps = max(1, args.reps)
     pts_nominal = list(wl.bernoulli) if wl.bernoulli else list(wl.rhos)
