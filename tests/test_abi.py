@@ -76,6 +76,28 @@ def _inputs(L, **kw):
                     base["scale"], base.get("k_cur"), base.get("v_cur"))
 
 
+def _plan_bytes(units, splits, G, D):
+    """Workspace of a plan with `splits` splits per unit: ticket words, partial
+    outputs and (max, sum) pairs, each rounded up to 256 bytes."""
+    up = lambda x: -(-x // 256) * 256
+    return 0 if splits <= 1 else up(units * 4) + up(units * splits * G * D * 4) + up(units * splits * G * 2 * 4)
+
+
+@pytest.mark.parametrize("L_,B,Hq,Hkv,D,n,s,w,splits", [
+    (1, 1, 32, 8, 128, 32768, 4, 1024, 7),      # one-layer Local, Llama shape: 66 blocks in splits of 10
+    (1, 1, 16, 8, 128, 131072, 4, 2048, 13),    # one-layer Local, decoder shape: 130 blocks in splits of 10
+    (1, 1, 16, 8, 128, 4140, 0, 0, 15),         # one-layer Full over 4,140 positions: at most 16 splits
+    (1, 1, 32, 8, 128, 32768, 0, 0, 32),        # one-layer Full over 32,768: 32 splits of 64 blocks
+    (32, 1, 32, 8, 128, 32768, 4, 1024, 1),     # the stacked call: one split per unit, no workspace
+])
+def test_automatic_split_plan(L, L_, B, Hq, Hkv, D, n, s, w, splits):
+    """The automatic plan (visible through the workspace it asks for): splits
+    of at least eight blocks for small calls, more than 16 only while each
+    keeps 64 blocks, one split per unit once the units fill the chip."""
+    shape = L.Shape(L_, B, Hq, Hkv, D, -(-n // 16), n, 1000, 0)
+    assert L.attn_workspace_size(shape, s, w) == _plan_bytes(L_ * B * Hkv, splits, Hq // Hkv, D)
+
+
 def test_local_rejects_bad_arguments_without_launching(L):
     s = _shape(L, split_blocks=2)           # several splits per request: a workspace is required
     ws_bytes = L.attn_workspace_size(s, 4, 16)
