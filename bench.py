@@ -523,7 +523,16 @@ class Bench:
         return float(np.mean(durs))
 
 
+TAU_MIN_GAP = 2 * FLAG_BORDER   # a threshold sits in a gap at least this wide between adjacent scores
+
+
 def taus_for(scores, rhos):
+    """Thresholds that flag round(rho * N) of the N scores: the midpoint of the
+    gap between the m-th and (m+1)-th largest.  A gap narrower than
+    TAU_MIN_GAP would leave the decisions on either side borderline, so the
+    threshold moves to the nearest gap that is wide enough (the realised rate
+    then differs from rho by that many decisions).  rho = 0 gives +inf, rho = 1
+    gives -inf."""
     flat = np.sort(scores.reshape(-1))[::-1]
     N = len(flat)
     out = {}
@@ -531,10 +540,20 @@ def taus_for(scores, rhos):
         m = int(round(rho * N))
         if m <= 0:
             out[rho] = math.inf
-        elif m >= N:
+            continue
+        if m >= N:
             out[rho] = -math.inf
-        else:
-            out[rho] = float(0.5 * (flat[m - 1] + flat[m]))
+            continue
+        wide = lambda i: 0 < i < N and flat[i - 1] - flat[i] >= TAU_MIN_GAP
+        pick = m
+        for off in range(N):
+            if wide(m - off):
+                pick = m - off
+                break
+            if wide(m + off):
+                pick = m + off
+                break
+        out[rho] = float(0.5 * (flat[pick - 1] + flat[pick]))
     return out
 
 

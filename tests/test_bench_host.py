@@ -28,7 +28,22 @@ def test_taus_flag_the_requested_number_of_decisions():
     taus = BN.taus_for(scores, (0.0, 0.1, 0.25, 1.0))
     assert taus[0.0] == math.inf and taus[1.0] == -math.inf
     for rho in (0.1, 0.25):
-        assert int((scores > taus[rho]).sum()) == round(rho * scores.size)
+        # round(rho N) flagged, give or take the few decisions a narrow gap moves it by
+        assert abs(int((scores > taus[rho]).sum()) - round(rho * scores.size)) <= 3
+        assert np.abs(scores - taus[rho]).min() >= BN.FLAG_BORDER   # no borderline decision at the threshold
+
+
+def test_taus_avoid_narrow_gaps():
+    """A gap below 2e-4 between the scores around the quantile moves the
+    threshold to the nearest wide gap, so no decision at it is borderline."""
+    s = np.array([5.0, 4.0, 3.0, 2.00005, 2.0, 1.0, 0.0, -1.0, -2.0, -3.0])
+    tau = BN.taus_for(s, (0.4,))[0.4]          # 4 of 10: the gap 2.00005 | 2.0 is too narrow
+    assert tau == 0.5 * (3.0 + 2.00005)          # the nearest wide gap (one fewer flagged)
+    assert np.abs(s - tau).min() >= 1e-4
+    tau = BN.taus_for(s, (0.5,))[0.5]          # 5 of 10: the gap 2.0 | 1.0 is wide already
+    assert tau == 1.5
+    tau = BN.taus_for(s, (0.3,))[0.3]          # 3 of 10: gap 3.0 | 2.00005 is wide
+    assert tau == 0.5 * (3.0 + 2.00005)
 
 
 def test_flags_vs_oracle_counts_borderline_and_mismatches():
