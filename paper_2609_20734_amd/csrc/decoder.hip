@@ -118,9 +118,12 @@ __global__ __launch_bounds__(256) void dense_kernel(DenseArgs p) {
   // read element 0 again and weigh it by zero, so every load is unconditional
   // and the loads of successive chunks overlap.
   const int nchunks = (p.K + 511) / 512;
-  // about eight 16-byte weight loads in flight per lane
+  // about eight 16-byte weight loads in flight per lane; sixteen for the
+  // SwiGLU pair of a single request (few registers per load there, and the
+  // pair is the decoder's largest layer)
   constexpr int kRowsPerChunk = kSwiGLU ? 2 * R : R;
-  constexpr int kUnroll = kRowsPerChunk >= 8 ? 1 : 8 / kRowsPerChunk;
+  constexpr int kInFlight = kSwiGLU && T == 1 ? 16 : 8;
+  constexpr int kUnroll = kRowsPerChunk >= kInFlight ? 1 : kInFlight / kRowsPerChunk;
 #pragma unroll kUnroll
   for (int c = 0; c < nchunks; ++c) {
     const int k0 = c * 512 + 8 * lane;
