@@ -313,13 +313,18 @@ def test_selection_sizes_on_one_workspace(cur):
                 assert np.all(o[:, b] == -7.0) and np.all(ls[:, b] == -7.0)
 
 
-@pytest.mark.parametrize("cur", [False, True])
-def test_layer_stride_between_layers(cur):
+@pytest.mark.parametrize("cur,walk", [(False, False), (True, False), (True, True)])
+def test_layer_stride_between_layers(cur, walk):
     """layer_stride_kv: each layer's blocks start `stride` elements after the
     previous layer's (here the dense size plus padding, as in one allocation
     holding several layer groups).  Local and Full read the right layers and
-    match the oracle on the dense copies."""
-    pb = AttnProblem(57, 3, 4, 16, 4, 128, [70, 300, 1, 515], cur=cur, split_blocks=2)
+    match the oracle on the dense copies; `walk` takes a batch large enough
+    that Local's workgroups each walk all four layers of a (request, KV head)."""
+    if walk:
+        seq = np.random.default_rng(58).integers(1, 300, size=64).tolist()
+        pb = AttnProblem(58, 4, 64, 8, 8, 64, seq, cur=cur)
+    else:
+        pb = AttnProblem(57, 3, 4, 16, 4, 128, [70, 300, 1, 515], cur=cur, split_blocks=2)
     P = pb.P
     dense = pb.nb * pb.Hkv * 16 * pb.D
     stride = dense + 8 * 37
@@ -329,7 +334,7 @@ def test_layer_stride_between_layers(cur):
         k_pad[l * stride:l * stride + dense] = pb.dk[l].reshape(-1)
         v_pad[l * stride:l * stride + dense] = pb.dv[l].reshape(-1)
     shape = P.Shape(pb.L, pb.B, pb.Hq, pb.Hkv, pb.D, pb.shape.max_blocks_per_seq, pb.shape.max_seq_len, pb.nb,
-                    2, layer_stride_kv=stride)
+                    pb.shape.split_blocks, layer_stride_kv=stride)
     inp = P.inputs(pb.dq, k_pad, v_pad, pb.dtable, pb.dseq, pb.scale, pb.dkc, pb.dvc)
     for local in (True, False):
         out, lse = pb.new_out(np.nan)
