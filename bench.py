@@ -1126,7 +1126,7 @@ def main():
                     help="time whole steps of the synthetic decoder (tokens/s) instead of the attention path")
     ap.add_argument("--lengths", default="", help="--decoder: comma-separated context lengths")
     ap.add_argument("--decoder-steps", type=int, default=64, help="--decoder: timed steps per method")
-    ap.add_argument("--extra-configs", default="llama3-8b",
+    ap.add_argument("--extra-configs", default="llama3-8b,long,hybrid",
                     help="comma-separated workloads given a shortened run after the main one ('' for none)")
     ap.add_argument("--gate-only", action="store_true",
                     help="only the recall gate (both heads) plus a 1 GiB copy, for PMC profiling")
