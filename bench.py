@@ -121,10 +121,18 @@ class StackState:
         self.ws_local = torch.zeros(P.attn_workspace_size(self.shape, loc_s, loc_w), dtype=torch.uint8, device=dev)
         self.ws_full = torch.zeros(P.attn_workspace_size(self.shape, 0, stack.native_window), dtype=torch.uint8,
                                    device=dev)
+        self.k_ring = self.v_ring = None
+
+    def make_rings(self, P, dev):
+        """Direct-ring Local workspace of this layer group (filled by Bench.fill_rings)."""
+        import torch
+        n = P.ring_elements(self.shape, *self.local_args)
+        self.k_ring = torch.empty(n, dtype=torch.int16, device=dev)
+        self.v_ring = torch.empty(n, dtype=torch.int16, device=dev)
 
 
 class Bench:
-    def __init__(self, wl, head, seed, steps, split_blocks=0, growth=0):
+    def __init__(self, wl, head, seed, steps, split_blocks=0, growth=0, local="ring"):
         import torch
 
         import oda_synth as S
@@ -147,6 +155,12 @@ class Bench:
         self.dseq = torch.from_numpy(seq).to(dev)
         self.stacks = [StackState(P, wl, st, self.dseq, self.dtable, nb, mb, int(seq.max()) + growth, seed, dev,
                                   split_blocks) for st in wl.stacks]
+        # Local reads the direct-ring workspace (App. A.5), or the paged cache
+        self.local = local
+        if local == "ring":
+            for st in self.stacks:
+                st.make_rings(P, dev)
+            self.fill_rings()
         # gate
         h, e, l = S.gate_inputs(seed, steps, B, wl.d_model)
         self.h = torch.from_numpy(h).to(dev)
@@ -171,6 +185,32 @@ class Bench:
     def flush(self):
         self.flush_buf.max()
 
+    def fill_rings(self):
+        """(Re)fill every layer group's rings from the paged cache at the current lengths."""
+        for st in self.stacks:
+            if st.k_ring is not None:
+                self.P.ring_fill(st.shape, st.k, st.v, self.dtable, self.dseq, *st.local_args, st.k_ring, st.v_ring)
+
+    def local_call(self, st, layer=None, k_cur=None, v_cur=None, ws=None):
+        """The pre-marshalled Local call of a layer group (all its layers, or one
+        layer with a one-layer shape), through the rings or the paged cache."""
+        P = self.P
+        scale = 1.0 / math.sqrt(self.wl.head_dim)
+        shape, q, out, lse, kr, vr, k, v = st.shape, st.q, st.out, st.lse, st.k_ring, st.v_ring, st.k, st.v
+        if layer is not None:
+            s = st.shape
+            shape = P.Shape(1, s.batch, s.num_q_heads, s.num_kv_heads, s.head_dim, s.max_blocks_per_seq,
+                            s.max_seq_len, s.num_blocks, s.split_blocks)
+            q, out, lse, k, v = q[layer], out[layer], lse[layer], k[layer], v[layer]
+            if kr is not None:
+                kr, vr = kr.view(st.stack.num_layers, -1)[layer], vr.view(st.stack.num_layers, -1)[layer]
+        ws = st.ws_local if ws is None else ws
+        if self.local == "ring":
+            return P.prepare_local_ring(shape, P.inputs(q, None, None, None, self.dseq, scale, k_cur, v_cur), kr, vr,
+                                        *st.local_args, out, lse, ws)
+        return P.prepare_local(shape, P.inputs(q, k, v, self.dtable, self.dseq, scale, k_cur, v_cur),
+                               *st.local_args, out, lse, ws)
+
     def set_head(self, head):
         """Recall head used by the steps: the App. A.2 form ("paper") or the MLP stand-in."""
         import torch
@@ -190,7 +230,7 @@ class Bench:
         gated_only: the Full retry covers only the gated layer groups (natively
         windowed layers keep their Local result, which is already native)."""
         P = self.P
-        local = [P.prepare_local(s.shape, s.inp, *s.local_args, s.out, s.lse, s.ws_local) for s in self.stacks]
+        local = [self.local_call(s) for s in self.stacks]
         full = [P.prepare_full(s.shape, s.inp, s.stack.native_window, None, self.work, self.n_work, s.out, s.lse,
                                s.ws_full) for s in self.stacks if s.stack.gated or not gated_only]
         steps = []
@@ -225,11 +265,16 @@ class Bench:
         ws_commit = torch.zeros(P.commit_workspace_size(self.stacks[-1].shape), dtype=torch.uint8, device=self.dev)
         res = []
 
+        def reset():
+            # lengths back to the start; rings rebuilt (commits past the start overwrote ring blocks the
+            # window at the start still reads), the paged cache below the start is intact
+            self.dseq.copy_(seq0)
+            self.fill_rings()
+
         def one_period(forced):
             for t in range(period):
                 for st, (kl, vl, kf, vf) in zip(self.stacks, cands):
-                    inp = P.inputs(st.q, st.k, st.v, self.dtable, self.dseq, scale, kl[t], vl[t])
-                    P.local_decode_attn(st.shape, inp, *st.local_args, st.out, st.lse, st.ws_local)
+                    self.local_call(st, k_cur=kl[t], v_cur=vl[t])()
                 P.recall_gate(self.gate, B, self.h[t % self.K], self.e[t % self.K], self.l[t % self.K], 0.0,
                               forced[t], self.score, self.flags, self.work, self.n_work, self.counter, self.ws_gate)
                 for st, (kl, vl, kf, vf) in zip(self.stacks, cands):
@@ -237,17 +282,22 @@ class Bench:
                     P.full_decode_attn(st.shape, inp, st.stack.native_window, None, self.work, self.n_work,
                                        st.out, st.lse, st.ws_full)
                 for i, (st, (kl, vl, kf, vf)) in enumerate(zip(self.stacks, cands)):
-                    P.commit_kv(st.shape, st.k, st.v, self.dtable, self.dseq, kl[t], vl[t], kf[t], vf[t],
-                                self.flags, i == len(self.stacks) - 1, ws_commit)
+                    if st.k_ring is not None:
+                        P.commit_kv_ring(st.shape, st.k, st.v, self.dtable, self.dseq, kl[t], vl[t], kf[t], vf[t],
+                                         self.flags, i == len(self.stacks) - 1, ws_commit, st.k_ring, st.v_ring,
+                                         *st.local_args)
+                    else:
+                        P.commit_kv(st.shape, st.k, st.v, self.dtable, self.dseq, kl[t], vl[t], kf[t], vf[t],
+                                    self.flags, i == len(self.stacks) - 1, ws_commit)
 
         for k in firsts:
             sched = np.stack([S.periodic_schedule(period, k)] * B, axis=1).astype(np.int32)
             forced = torch.from_numpy(sched).to(self.dev)
             # eager: launched from the host every period
-            self.dseq.copy_(seq0)
+            reset()
             one_period(forced)
             torch.cuda.synchronize()
-            self.dseq.copy_(seq0)
+            reset()
             self.counter.zero_()
             a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
@@ -258,15 +308,15 @@ class Bench:
             eager_us = a.elapsed_time(b_) * 1e3 / (reps * period)
             recalled = int(self.counter.item())
             # graph: the whole period captured once, replayed
-            self.dseq.copy_(seq0)
+            reset()
             g = torch.cuda.CUDAGraph()
             torch.cuda.synchronize()
             with torch.cuda.graph(g):
                 one_period(forced)
-            self.dseq.copy_(seq0)
+            reset()
             g.replay()
             torch.cuda.synchronize()
-            self.dseq.copy_(seq0)
+            reset()
             torch.cuda.synchronize()
             a.record()
             for _ in range(reps):
@@ -280,7 +330,7 @@ class Bench:
             log(f"[bench] decode loop first {k}/{period} Full: eager {eager_us:.1f} us/step, "
                 f"graph {graph_us:.1f} us/step, recalled {recalled}/{reps * period * B}")
             del g
-        self.dseq.copy_(seq0)
+        reset()
         return res
 
     def full_calls(self):
@@ -350,9 +400,11 @@ class Bench:
 
     def local_layout(self, reps=20):
         """Local attention alone (every stack, cold) reading the window through
-        the permuted block table and through a contiguous one (identity table,
-        same cache, same lengths): the cost of scattered paged-window reads,
-        which decides whether a contiguous ring workspace for Local would pay."""
+        the permuted block table, through a contiguous one (identity table,
+        same cache, same lengths), and from the direct-ring workspace
+        (oda_local_decode_attn_ring over rings filled from the same cache: no
+        table at all); then the same for one layer of the first stack, where
+        the table lookup is a larger share of a call."""
         import oda_synth as S
         torch, P = self.torch, self.P
         seq = self.seq_host + self.growth
@@ -366,6 +418,35 @@ class Bench:
             calls = [P.prepare_local(st.shape, P.inputs(st.q, st.k, st.v, table, self.dseq, scale), *st.local_args,
                                      st.out, st.lse, st.ws_local) for st in self.stacks]
             res[f"{name}_us"] = self.kernel_time(calls, reps, cold=True)
+        rings = []
+        for st in self.stacks:
+            if st.k_ring is not None:
+                rings.append((st.k_ring, st.v_ring))
+                continue
+            n = P.ring_elements(st.shape, *st.local_args)
+            kr = torch.empty(n, dtype=torch.int16, device=self.dev)
+            vr = torch.empty(n, dtype=torch.int16, device=self.dev)
+            P.ring_fill(st.shape, st.k, st.v, self.dtable, self.dseq, *st.local_args, kr, vr)
+            rings.append((kr, vr))
+        calls = [P.prepare_local_ring(st.shape, P.inputs(st.q, None, None, None, self.dseq, scale), kr, vr,
+                                      *st.local_args, st.out, st.lse, st.ws_local)
+                 for st, (kr, vr) in zip(self.stacks, rings)]
+        res["ring_us"] = self.kernel_time(calls, reps, cold=True)
+        res["ring_bytes"] = int(sum(2 * r[0].numel() * 2 for r in rings))
+        # one layer of the first stack (the per-layer launch mode's Local call)
+        st, (kr, vr) = self.stacks[0], rings[0]
+        sh = st.shape
+        one = P.Shape(1, sh.batch, sh.num_q_heads, sh.num_kv_heads, sh.head_dim, sh.max_blocks_per_seq,
+                      sh.max_seq_len, sh.num_blocks, sh.split_blocks)
+        ws1 = torch.zeros(max(256, P.attn_workspace_size(one, *st.local_args)), dtype=torch.uint8, device=self.dev)
+        paged1 = P.prepare_local(one, P.inputs(st.q[0], st.k, st.v, self.dtable, self.dseq, scale), *st.local_args,
+                                 st.out[0], st.lse[0], ws1)
+        ring1 = P.prepare_local_ring(one, P.inputs(st.q[0], None, None, None, self.dseq, scale), kr, vr,
+                                     *st.local_args, st.out[0], st.lse[0], ws1)
+        res["one_layer_permuted_us"] = self.kernel_time([paged1], reps, cold=True)
+        res["one_layer_ring_us"] = self.kernel_time([ring1], reps, cold=True)
+        del rings, calls, kr, vr
+        torch.cuda.empty_cache()
         return res
 
     # -- per-layer launch mode --------------------------------------------------
@@ -395,8 +476,7 @@ class Bench:
         P = self.P
         calls = []
         for st, sh, ws_l, _, ins in self._layer_state():
-            calls += [P.prepare_local(sh, inp, *st.local_args, st.out[l], st.lse[l], ws_l)
-                      for l, inp in enumerate(ins)]
+            calls += [self.local_call(st, layer=l, ws=ws_l) for l in range(len(ins))]
         calls.append(P.prepare_gate(self.gate, self.wl.batch, self.h_stage, self.e_stage, self.l_stage, tau,
                                     self.f_stage if forced is not None else None, self.score, self.flags,
                                     self.work, self.n_work, self.counter, self.ws_gate))
@@ -927,7 +1007,7 @@ def extra_config(name, args):
     wl = WL.ALL[name]
     K = wl.steps
     oracle = oracle_gate_scores(wl, args.seed, K)
-    b = Bench(wl, "paper", args.seed, K)
+    b = Bench(wl, "paper", args.seed, K, local="paged" if args.local_paged else "ring")
     b.oracle_scores = oracle
     sub = copy.copy(args)
     sub.no_warm = True
@@ -944,7 +1024,8 @@ def extra_config(name, args):
     roof["frac"] = roof["achieved"] / roof["peak"]
     out = dict(workload=f"{wl.name}: {wl.num_layers} layers, B={wl.batch}, {wl.num_q_heads}q/{wl.num_kv_heads}kv heads, "
                         f"D={wl.head_dim}, n={'/'.join(str(x) for x in sorted(set(b.seq_host.tolist()))[:4])}, "
-                        f"W={wl.stacks[-1].local_window}, s={wl.stacks[-1].local_sink}, paper recall head "
+                        f"W={wl.stacks[-1].local_window}, s={wl.stacks[-1].local_sink}, Local from the "
+                        f"{'paged cache' if args.local_paged else 'direct-ring workspace'}, paper recall head "
                         f"{wl.d_model}->{wl.d_hidden}->1, cold",
                steps=K, reps=args.reps, always_full_us=round(full_us, 3),
                sweep=[rounded(e) for e in sweep], roofline=rounded(roof))
@@ -1126,6 +1207,8 @@ def main():
                     help="time whole steps of the synthetic decoder (tokens/s) instead of the attention path")
     ap.add_argument("--lengths", default="", help="--decoder: comma-separated context lengths")
     ap.add_argument("--decoder-steps", type=int, default=64, help="--decoder: timed steps per method")
+    ap.add_argument("--local-paged", action="store_true",
+                    help="Local reads the paged cache through the block table instead of the direct-ring workspace")
     ap.add_argument("--extra-configs", default="llama3-8b,long,hybrid",
                     help="comma-separated workloads given a shortened run after the main one ('' for none)")
     ap.add_argument("--gate-only", action="store_true",
@@ -1165,7 +1248,8 @@ def main():
 
     import torch
     b = Bench(wl, args.head, args.seed, K, args.split_blocks,
-              growth=0 if (args.no_loop or args.roofline_only) else 16 * 8)
+              growth=0 if (args.no_loop or args.roofline_only) else 16 * 8,
+              local="paged" if args.local_paged else "ring")
     P = b.P
     b.oracle_scores = oracle_scores
     local_b, gate_b, full_b = bytes_for(wl, b.seq_host, None, args.head)
@@ -1175,8 +1259,7 @@ def main():
         # dispatch order (the counter summaries rely on it): 1 + R Local launches,
         # 1 + R empty Full launches (list of zero requests), 1 + R roofline
         # launches (Full over every request), then three 1 GiB copies
-        t_loc = b.kernel_time([P.prepare_local(s.shape, s.inp, *s.local_args, s.out, s.lse, s.ws_local)
-                               for s in b.stacks], reps=ROOFLINE_REPS, cold=True)
+        t_loc = b.kernel_time([b.local_call(s) for s in b.stacks], reps=ROOFLINE_REPS, cold=True)
         b.n_work.zero_()
         t_empty = b.kernel_time([P.prepare_full(s.shape, s.inp, s.stack.native_window, None, b.work, b.n_work,
                                                 s.out, s.lse, s.ws_full) for s in b.stacks],
@@ -1221,7 +1304,9 @@ def main():
     loop = [] if args.no_loop else b.decode_loop()
     layout = b.local_layout()
     log(f"[bench] Local alone, cold: permuted block table {layout['permuted_us']:.1f} us, "
-        f"contiguous table {layout['contiguous_us']:.1f} us")
+        f"contiguous table {layout['contiguous_us']:.1f} us, direct ring {layout['ring_us']:.1f} us "
+        f"(rings {layout['ring_bytes'] / 1e9:.2f} GB); one layer: permuted {layout['one_layer_permuted_us']:.2f} us, "
+        f"ring {layout['one_layer_ring_us']:.2f} us")
     sinks = b.local_sinks()
     log(f"[bench] Local alone, cold: s={sinks['n_sink']} {sinks['sinks_us']:.1f} us, s=0 {sinks['no_sinks_us']:.1f} us")
 
@@ -1258,10 +1343,13 @@ def main():
                                   if wl.seq_range else f"n={'/'.join(str(x) for x in nset[:4])}"
                                   f"{'...' if len(nset) > 4 else ''}") + ", "
                                f"W={wl.stacks[-1].local_window}, s={wl.stacks[-1].local_sink}, paged bf16 KV "
-                               f"(block 16, permuted), {args.head} recall head {wl.d_model}->{wl.d_hidden}->1, "
+                               f"(block 16, permuted), Local from the "
+                               f"{'paged cache' if args.local_paged else 'direct-ring workspace'}, "
+                               f"{args.head} recall head {wl.d_model}->{wl.d_hidden}->1, "
                                f"{head_ent['mode'] + ' ' if head_ent else ''}rho={head_ent['rho'] if head_ent else 1.0}, "
                                f"cold (Infinity Cache flushed between steps)",
-                   "head": args.head, "seed": args.seed, "split_blocks": args.split_blocks},
+                   "head": args.head, "seed": args.seed, "split_blocks": args.split_blocks,
+                   "local": "paged" if args.local_paged else "ring"},
         "GBps": round(head_ent["GBps"], 1) if head_ent else None,
         "always_full_us": round(full_us, 3),
         "always_full_us_reps": [round(f["us_mean"], 3) for f in fulls],

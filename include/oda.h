@@ -307,6 +307,59 @@ oda_status oda_commit_kv(const oda_attn_shape *shape, uint16_t *k_cache, uint16_
                          hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * Direct-ring Local (App. A.5: the Local path reads a contiguous workspace
+ * holding the attention sinks and the recent window, with the current token
+ * supplied separately, instead of the paged cache).  Per (layer, request, KV
+ * head) unit, a ring of whole 16-position blocks in the cache's block
+ * layouts.  For sinks s and window w:
+ *   SB = ceil(s / 16) sink blocks, then RB = ceil(w / 16) + 2 ring blocks;
+ *   logical block j of a request is held in ring block j if j < SB, else in
+ *   ring block SB + (j mod RB)
+ *   k_ring  bf16 [L][B][SB + RB][Hkv][D/8][16][8]
+ *   v_ring  bf16 [L][B][SB + RB][Hkv][D][16]
+ * RB blocks keep every block a Local call reads until the window has moved
+ * past it, so a ring filled once (oda_ring_fill) and then kept current by the
+ * commit (oda_commit_kv_ring) serves every later step.  A Local call through
+ * the ring reads no block table and the same positions, in the same order,
+ * as oda_local_decode_attn: the results are bit-identical.  Ring slots of
+ * positions not yet committed may hold anything; no call reads them.  n_sink
+ * and window must be the same in every call on a ring.
+ * ------------------------------------------------------------------------- */
+
+/* bf16 elements of each of k_ring and v_ring (host out). */
+oda_status oda_ring_elements(const oda_attn_shape *shape, int32_t n_sink, int32_t window, int64_t *elements);
+
+/* Fill the rings from the paged cache (one launch): every sink block, and in
+ * every ring block the latest logical block j <= (seq_lens[b] - 1) / 16 that
+ * maps to it, copied whole.  A request whose length is outside
+ * [1, max_seq_len], or a table entry outside [0, num_blocks), leaves the ring
+ * blocks concerned as they are.  Uses the same shape fields as
+ * oda_local_decode_attn (layer_stride_kv included). */
+oda_status oda_ring_fill(const oda_attn_shape *shape, const uint16_t *k_cache, const uint16_t *v_cache,
+                         const int32_t *block_table, const int32_t *seq_lens, int32_t n_sink, int32_t window,
+                         uint16_t *k_ring, uint16_t *v_ring, hipStream_t stream);
+
+/* oda_local_decode_attn reading the rings: in->q, seq_lens, k_cur / v_cur
+ * (the uncommitted candidate, or NULL when position n_b - 1 is in the ring)
+ * and scale as there; in->k_cache, v_cache and block_table are not read (may
+ * be NULL).  Same workspace (oda_attn_workspace_size(shape, n_sink, window)),
+ * same outputs, bit for bit. */
+oda_status oda_local_decode_attn_ring(const oda_attn_shape *shape, const oda_attn_inputs *in,
+                                      const uint16_t *k_ring, const uint16_t *v_ring, int32_t n_sink,
+                                      int32_t window, float *out, float *lse, void *workspace,
+                                      size_t workspace_bytes, hipStream_t stream);
+
+/* oda_commit_kv that also writes each committed position into the rings
+ * (ring block of logical block (n_b - 1) / 16, slot (n_b - 1) % 16), in the
+ * same launch.  The rings' shape is the commit's (L, B, Hkv, D). */
+oda_status oda_commit_kv_ring(const oda_attn_shape *shape, uint16_t *k_cache, uint16_t *v_cache,
+                              const int32_t *block_table, int32_t *seq_lens, const uint16_t *k_local,
+                              const uint16_t *v_local, const uint16_t *k_full, const uint16_t *v_full,
+                              const int32_t *flags, int32_t advance, void *workspace, size_t workspace_bytes,
+                              uint16_t *k_ring, uint16_t *v_ring, int32_t n_sink, int32_t window,
+                              hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * The decoder around the hot path (the backbone f_theta of §2.1 that Local and
  * Full share; App. A.6's cost model).  A pre-norm decoder layer is, per request:
  *   qkv = W_qkv . RMSNorm(h)              oda_dense_bf16 (gain = input norm)

@@ -36,6 +36,7 @@ EXPORTED = ("oda_attn_workspace_size", "oda_local_decode_attn", "oda_full_decode
             "oda_local_decode_attn_qkv", "oda_full_decode_attn_qkv",
             "oda_gate_param_count", "oda_gate_workspace_size", "oda_recall_gate", "oda_recall_gate_static",
             "oda_commit_workspace_size", "oda_commit_kv",
+            "oda_ring_elements", "oda_ring_fill", "oda_local_decode_attn_ring", "oda_commit_kv_ring",
             "oda_dense_bf16", "oda_qk_norm_rope", "oda_embed_bf16", "oda_copy_rows", "oda_rms_norm_rows",
             "oda_argmax", "oda_stream_read", "oda_status_string", "oda_last_error")
 
@@ -116,6 +117,16 @@ _lib.oda_commit_kv.argtypes = [_P(AttnShape), ctypes.c_void_p, ctypes.c_void_p, 
                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
 _lib.oda_commit_kv.restype = ctypes.c_int
+_lib.oda_ring_elements.argtypes = [_P(AttnShape), ctypes.c_int32, ctypes.c_int32, _P(ctypes.c_int64)]
+_lib.oda_ring_elements.restype = ctypes.c_int
+_lib.oda_ring_fill.argtypes = [_P(AttnShape), _V, _V, _V, _V, ctypes.c_int32, ctypes.c_int32, _V, _V, _V]
+_lib.oda_ring_fill.restype = ctypes.c_int
+_lib.oda_local_decode_attn_ring.argtypes = [_P(AttnShape), _P(AttnInputs), _V, _V, ctypes.c_int32, ctypes.c_int32,
+                                            _V, _V, _V, ctypes.c_size_t, _V]
+_lib.oda_local_decode_attn_ring.restype = ctypes.c_int
+_lib.oda_commit_kv_ring.argtypes = [_P(AttnShape), _V, _V, _V, _V, _V, _V, _V, _V, _V, ctypes.c_int32, _V,
+                                    ctypes.c_size_t, _V, _V, ctypes.c_int32, ctypes.c_int32, _V]
+_lib.oda_commit_kv_ring.restype = ctypes.c_int
 _lib.oda_dense_bf16.argtypes = [_P(DenseDesc), ctypes.c_int32, _V, _V, _V, _V, _V, _V]
 _lib.oda_dense_bf16.restype = ctypes.c_int
 _lib.oda_qk_norm_rope.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _V, _V, _V,
@@ -278,6 +289,35 @@ def commit_kv(shape: Shape, k_cache, v_cache, block_table, seq_lens, k_local, v_
                               _nbytes(workspace, workspace_bytes), _stream(stream)))
 
 
+def ring_elements(shape: Shape, n_sink: int, window: int) -> int:
+    out = ctypes.c_int64(0)
+    _check(_lib.oda_ring_elements(ctypes.byref(shape.c()), n_sink, window, ctypes.byref(out)))
+    return out.value
+
+
+def ring_fill(shape: Shape, k_cache, v_cache, block_table, seq_lens, n_sink: int, window: int, k_ring, v_ring,
+              stream=None) -> None:
+    _check(_lib.oda_ring_fill(ctypes.byref(shape.c()), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+                              _ptr(seq_lens), n_sink, window, _ptr(k_ring), _ptr(v_ring), _stream(stream)))
+
+
+def local_decode_attn_ring(shape: Shape, inp: AttnInputs, k_ring, v_ring, n_sink: int, window: int, out, lse,
+                           workspace, workspace_bytes: int | None = None, stream=None) -> None:
+    _check(_lib.oda_local_decode_attn_ring(ctypes.byref(shape.c()), ctypes.byref(inp), _ptr(k_ring), _ptr(v_ring),
+                                           n_sink, window, _ptr(out), _ptr(lse), _ptr(workspace),
+                                           _nbytes(workspace, workspace_bytes), _stream(stream)))
+
+
+def commit_kv_ring(shape: Shape, k_cache, v_cache, block_table, seq_lens, k_local, v_local, k_full=None,
+                   v_full=None, flags=None, advance: bool = True, workspace=None, k_ring=None, v_ring=None,
+                   n_sink: int = 0, window: int = 1, workspace_bytes: int | None = None, stream=None) -> None:
+    _check(_lib.oda_commit_kv_ring(ctypes.byref(shape.c()), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+                                   _ptr(seq_lens), _ptr(k_local), _ptr(v_local), _ptr(k_full), _ptr(v_full),
+                                   _ptr(flags), 1 if advance else 0, _ptr(workspace),
+                                   _nbytes(workspace, workspace_bytes), _ptr(k_ring), _ptr(v_ring), n_sink, window,
+                                   _stream(stream)))
+
+
 def dense_desc(in_features: int, out_features: int, mode: int, weight, norm_gain=None,
                rms_eps: float = 1e-6) -> DenseDesc:
     """The C dense-layer description; it keeps the weight and gain tensors alive."""
@@ -352,6 +392,14 @@ def prepare_local(shape: Shape, inp: AttnInputs, n_sink: int, window: int, out, 
     args = (ctypes.byref(cs), ctypes.byref(inp), n_sink, window, _ptr(out), _ptr(lse), _ptr(workspace),
             _nbytes(workspace, workspace_bytes), _stream(stream))
     return Call(_lib.oda_local_decode_attn, args, (cs, inp, out, lse, workspace))
+
+
+def prepare_local_ring(shape: Shape, inp: AttnInputs, k_ring, v_ring, n_sink: int, window: int, out, lse, workspace,
+                       workspace_bytes: int | None = None, stream=None) -> Call:
+    cs = shape.c()
+    args = (ctypes.byref(cs), ctypes.byref(inp), _ptr(k_ring), _ptr(v_ring), n_sink, window, _ptr(out), _ptr(lse),
+            _ptr(workspace), _nbytes(workspace, workspace_bytes), _stream(stream))
+    return Call(_lib.oda_local_decode_attn_ring, args, (cs, inp, k_ring, v_ring, out, lse, workspace))
 
 
 def qkv_prep(qkv, q_gain, k_gain, rms_eps: float, rope_theta: float, k_out=None, v_out=None) -> QkvPrep:

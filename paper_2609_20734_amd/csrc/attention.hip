@@ -101,6 +101,12 @@ struct AttnArgs {
   uint16_t* v_out;       // [B][Hkv][D]
   double rope_theta;
   float rms_eps;
+  // direct-ring Local: the window is read from per-unit rings of whole blocks
+  // (k_ring [L][B][SB + RB][Hkv][D/8][16][8], v_ring alike) instead of the
+  // paged cache; logical block j sits in ring block j (j < SB) or SB + j % RB
+  const uint16_t* k_ring;   // NULL: read the paged cache through the block table
+  const uint16_t* v_ring;
+  int32_t ring_sb, ring_rb;
 };
 
 // Where a unit's query rows and current candidate come from: global memory,
@@ -265,17 +271,22 @@ struct Run {
   Geometry geo;
   const uint16_t* kbase;
   const uint16_t* vbase;
-  const int32_t* bt;
+  const int32_t* bt;        // NULL: blocks come from the unit's ring (ring_sb, ring_rb)
   int64_t blk_stride;
   int64_t nblocks;
   int v_lo, v_hi;
+  int ring_sb, ring_rb;
 };
 
 // Physical blocks of 64 consecutive virtual blocks, one per lane.  An entry
 // outside [0, num_blocks) reads block 0 instead and sets `bad`.
 __device__ __forceinline__ int table_chunk(const Run& r, int chunk, int lane, int& bad) {
   const int v = r.v_lo + chunk * 64 + lane;
-  const int e = v < r.v_hi ? r.bt[logical_block(r.geo, v)] : 0;
+  int e = 0;
+  if (v < r.v_hi) {
+    const int lb = logical_block(r.geo, v);
+    e = r.bt != nullptr ? r.bt[lb] : (lb < r.ring_sb ? lb : r.ring_sb + lb % r.ring_rb);
+  }
   const bool ok = e >= 0 && e < r.nblocks;
   bad |= ok ? 0 : 1;
   return ok ? e : 0;
@@ -547,11 +558,21 @@ __device__ __forceinline__ void run_unit(const AttnArgs& a, Run& r, int l, int b
   const int j = lane >> 4;
   const int G = a.G;
   const int64_t head_elems = (int64_t)kBlock * D;
-  r.kbase = a.k_cache + (int64_t)l * a.kv_layer_stride + (int64_t)g * head_elems;
-  r.vbase = a.v_cache + (int64_t)l * a.kv_layer_stride + (int64_t)g * head_elems;
   r.blk_stride = (int64_t)a.Hkv * head_elems;
-  r.nblocks = a.num_blocks;
-  r.bt = a.block_table + (int64_t)b * a.MB;
+  r.ring_sb = a.ring_sb;
+  r.ring_rb = a.ring_rb;
+  if (a.k_ring != nullptr) {
+    const int64_t unit0 = ((int64_t)l * a.B + b) * (a.ring_sb + a.ring_rb) * r.blk_stride + (int64_t)g * head_elems;
+    r.kbase = a.k_ring + unit0;
+    r.vbase = a.v_ring + unit0;
+    r.nblocks = a.ring_sb + a.ring_rb;
+    r.bt = nullptr;
+  } else {
+    r.kbase = a.k_cache + (int64_t)l * a.kv_layer_stride + (int64_t)g * head_elems;
+    r.vbase = a.v_cache + (int64_t)l * a.kv_layer_stride + (int64_t)g * head_elems;
+    r.nblocks = a.num_blocks;
+    r.bt = a.block_table + (int64_t)b * a.MB;
+  }
 
   f32x4 o[NT];
 #pragma unroll
@@ -984,7 +1005,8 @@ oda_status launch(const AttnArgs& args, const Plan& plan, hipStream_t stream) {
 oda_status run_attention(const oda_attn_shape* s, const oda_attn_inputs* in, bool local, int n_sink, int window,
                          int select, const int32_t* flags, const int32_t* work_list, const int32_t* n_work,
                          float* out, float* lse, void* ws, size_t ws_bytes, hipStream_t stream,
-                         const oda_qkv_prep* prep = nullptr) {
+                         const oda_qkv_prep* prep = nullptr, const uint16_t* k_ring = nullptr,
+                         const uint16_t* v_ring = nullptr) {
   Plan plan;
   // Local attends every request; Full is sized for the fewest selected (one)
   make_plan(s, n_sink, window, local ? s->batch : 1, &plan);
@@ -1029,6 +1051,11 @@ oda_status run_attention(const oda_attn_shape* s, const oda_attn_inputs* in, boo
   a.v_out = prep ? prep->v_out : nullptr;
   a.rope_theta = prep ? prep->rope_theta : 0.0;
   a.rms_eps = prep ? prep->rms_eps : 0.f;
+  a.k_ring = k_ring;
+  a.v_ring = v_ring;
+  const oda::RingGeometry rg = oda::ring_geometry(n_sink, window > 0 ? window : 1);
+  a.ring_sb = k_ring ? rg.sink_blocks : 0;
+  a.ring_rb = k_ring ? rg.ring_blocks : 1;
   a.bps = plan.bps;
   a.max_splits = plan.max_splits;
   a.dyn_splits = plan.dyn;
@@ -1120,4 +1147,38 @@ extern "C" oda_status oda_full_decode_attn(const oda_attn_shape* shape, const od
   const int select = work_list ? kSelList : (flags ? kSelFlags : kSelAll);
   return run_attention(shape, in, false, 0, native_window, select, flags, work_list, n_work, out, lse, workspace,
                        workspace_bytes, stream);
+}
+
+extern "C" oda_status oda_ring_elements(const oda_attn_shape* shape, int32_t n_sink, int32_t window,
+                                        int64_t* elements) {
+  oda_status st = check_shape(shape);
+  if (st != ODA_OK) return st;
+  if (elements == nullptr) return oda::fail(ODA_ERR_NULL, "elements is NULL");
+  if (n_sink < 0 || window < 1) return oda::fail(ODA_ERR_SHAPE, "n_sink >= 0 and window >= 1 required");
+  const oda::RingGeometry rg = oda::ring_geometry(n_sink, window);
+  *elements = (int64_t)shape->num_layers * shape->batch * (rg.sink_blocks + rg.ring_blocks) * shape->num_kv_heads *
+              kBlock * shape->head_dim;
+  return oda::ok();
+}
+
+extern "C" oda_status oda_local_decode_attn_ring(const oda_attn_shape* shape, const oda_attn_inputs* in,
+                                                const uint16_t* k_ring, const uint16_t* v_ring, int32_t n_sink,
+                                                int32_t window, float* out, float* lse, void* workspace,
+                                                size_t workspace_bytes, hipStream_t stream) {
+  oda_status st = check_shape(shape);
+  if (st != ODA_OK) return st;
+  if (in == nullptr) return oda::fail(ODA_ERR_NULL, "inputs is NULL");
+  if (!in->q || !in->seq_lens || !out || !k_ring || !v_ring)
+    return oda::fail(ODA_ERR_NULL, "q, seq_lens, out, k_ring and v_ring are required");
+  if ((in->k_cur == nullptr) != (in->v_cur == nullptr))
+    return oda::fail(ODA_ERR_NULL, "k_cur and v_cur must both be NULL or both be set");
+  if (!oda::aligned(in->q, 16) || !oda::aligned(k_ring, 16) || !oda::aligned(v_ring, 16) || !oda::aligned(out, 16) ||
+      (in->k_cur && (!oda::aligned(in->k_cur, 16) || !oda::aligned(in->v_cur, 16))))
+    return oda::fail(ODA_ERR_SHAPE, "q, rings, k_cur, v_cur and out must be 16-byte aligned");
+  if (!(in->scale > 0.f) || !std::isfinite(in->scale))
+    return oda::fail(ODA_ERR_SHAPE, "scale must be finite and > 0");
+  if (n_sink < 0) return oda::fail(ODA_ERR_SHAPE, "n_sink must be >= 0");
+  if (window < 1) return oda::fail(ODA_ERR_SHAPE, "window must be >= 1 for Local attention");
+  return run_attention(shape, in, true, n_sink, window, kSelAll, nullptr, nullptr, nullptr, out, lse, workspace,
+                       workspace_bytes, stream, nullptr, k_ring, v_ring);
 }

@@ -34,6 +34,9 @@ struct CommitArgs {
   int32_t L, B, Hkv, D, MB;
   int32_t chunks;            // workgroups per request
   int32_t units_per_chunk;   // (layer, KV head) units per workgroup
+  uint16_t* k_ring;          // NULL, or the direct-ring Local rings [L][B][sb + rb][Hkv][..] (cache block layouts)
+  uint16_t* v_ring;
+  int32_t ring_sb, ring_rb;  // sink blocks, ring blocks
 };
 
 // Workgroup (b, c) moves the selected candidates of units [c upw, (c+1) upw)
@@ -66,20 +69,34 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
   const uint16_t* vs = full ? a.v_full : a.v_local;
   const int slot = pos & (kBlock - 1);
   const int groups = a.D / 8;
+  // the ring block holding this position (direct-ring Local): its sink block,
+  // or slot j mod rb of the ring
+  const int j = pos / kBlock;
+  const int nr = a.ring_sb + a.ring_rb;
+  const int rj = j < a.ring_sb ? j : a.ring_sb + j % a.ring_rb;
   for (int i = threadIdx.x; i < nu * groups; i += kThreads) {
     const int u = u0 + i / groups, d8 = i % groups;
     const int l = u / a.Hkv, g = u - l * a.Hkv;
     const int64_t src = (((int64_t)l * a.B + b) * a.Hkv + g) * a.D + d8 * 8;
     const int64_t dst = (int64_t)l * a.kv_layer_stride + (blk * a.Hkv + g) * kBlock * a.D;
-    *reinterpret_cast<u32x4*>(a.k_cache + dst + ((int64_t)d8 * kBlock + slot) * 8) =
-        *reinterpret_cast<const u32x4*>(ks + src);
+    const u32x4 k8 = *reinterpret_cast<const u32x4*>(ks + src);
+    *reinterpret_cast<u32x4*>(a.k_cache + dst + ((int64_t)d8 * kBlock + slot) * 8) = k8;
+    if (a.k_ring != nullptr) {
+      const int64_t rdst = ((((int64_t)l * a.B + b) * nr + rj) * a.Hkv + g) * kBlock * a.D;
+      *reinterpret_cast<u32x4*>(a.k_ring + rdst + ((int64_t)d8 * kBlock + slot) * 8) = k8;
+    }
   }
   for (int i = threadIdx.x; i < nu * a.D; i += kThreads) {
     const int u = u0 + i / a.D, d = i % a.D;
     const int l = u / a.Hkv, g = u - l * a.Hkv;
     const int64_t src = (((int64_t)l * a.B + b) * a.Hkv + g) * a.D + d;
     const int64_t dst = (int64_t)l * a.kv_layer_stride + (blk * a.Hkv + g) * kBlock * a.D;
-    a.v_cache[dst + (int64_t)d * kBlock + slot] = vs[src];
+    const uint16_t v1 = vs[src];
+    a.v_cache[dst + (int64_t)d * kBlock + slot] = v1;
+    if (a.v_ring != nullptr) {
+      const int64_t rdst = ((((int64_t)l * a.B + b) * nr + rj) * a.Hkv + g) * kBlock * a.D;
+      a.v_ring[rdst + (int64_t)d * kBlock + slot] = v1;
+    }
   }
   if (a.tickets == nullptr) return;
   __syncthreads();
@@ -117,11 +134,13 @@ extern "C" oda_status oda_commit_workspace_size(const oda_attn_shape* shape, siz
   return oda::ok();
 }
 
-extern "C" oda_status oda_commit_kv(const oda_attn_shape* shape, uint16_t* k_cache, uint16_t* v_cache,
-                                   const int32_t* block_table, int32_t* seq_lens, const uint16_t* k_local,
-                                   const uint16_t* v_local, const uint16_t* k_full, const uint16_t* v_full,
-                                   const int32_t* flags, int32_t advance, void* workspace, size_t workspace_bytes,
-                                   hipStream_t stream) {
+namespace {
+
+oda_status run_commit(const oda_attn_shape* shape, uint16_t* k_cache, uint16_t* v_cache, const int32_t* block_table,
+                      int32_t* seq_lens, const uint16_t* k_local, const uint16_t* v_local, const uint16_t* k_full,
+                      const uint16_t* v_full, const int32_t* flags, int32_t advance, void* workspace,
+                      size_t workspace_bytes, uint16_t* k_ring, uint16_t* v_ring, int32_t n_sink, int32_t window,
+                      hipStream_t stream) {
   oda_status st = check_commit_shape(shape);
   if (st != ODA_OK) return st;
   if (!k_cache || !v_cache || !block_table || !seq_lens || !k_local || !v_local)
@@ -157,6 +176,11 @@ extern "C" oda_status oda_commit_kv(const oda_attn_shape* shape, uint16_t* k_cac
   a.D = shape->head_dim;
   a.MB = shape->max_blocks_per_seq;
   a.NB = shape->num_blocks;
+  a.k_ring = k_ring;
+  a.v_ring = v_ring;
+  const oda::RingGeometry rg = oda::ring_geometry(n_sink, window);
+  a.ring_sb = k_ring ? rg.sink_blocks : 0;
+  a.ring_rb = k_ring ? rg.ring_blocks : 1;
   // enough workgroups per request that the launch covers the CUs, each with
   // at least one (layer, KV head) unit
   const int64_t units = (int64_t)a.L * a.Hkv;
@@ -170,4 +194,29 @@ extern "C" oda_status oda_commit_kv(const oda_attn_shape* shape, uint16_t* k_cac
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return oda::fail(ODA_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return oda::ok();
+}
+
+}  // namespace
+
+extern "C" oda_status oda_commit_kv(const oda_attn_shape* shape, uint16_t* k_cache, uint16_t* v_cache,
+                                   const int32_t* block_table, int32_t* seq_lens, const uint16_t* k_local,
+                                   const uint16_t* v_local, const uint16_t* k_full, const uint16_t* v_full,
+                                   const int32_t* flags, int32_t advance, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream) {
+  return run_commit(shape, k_cache, v_cache, block_table, seq_lens, k_local, v_local, k_full, v_full, flags, advance,
+                    workspace, workspace_bytes, nullptr, nullptr, 0, 1, stream);
+}
+
+extern "C" oda_status oda_commit_kv_ring(const oda_attn_shape* shape, uint16_t* k_cache, uint16_t* v_cache,
+                                        const int32_t* block_table, int32_t* seq_lens, const uint16_t* k_local,
+                                        const uint16_t* v_local, const uint16_t* k_full, const uint16_t* v_full,
+                                        const int32_t* flags, int32_t advance, void* workspace,
+                                        size_t workspace_bytes, uint16_t* k_ring, uint16_t* v_ring, int32_t n_sink,
+                                        int32_t window, hipStream_t stream) {
+  if (!k_ring || !v_ring) return oda::fail(ODA_ERR_NULL, "k_ring and v_ring are required");
+  if (!oda::aligned(k_ring, 16) || !oda::aligned(v_ring, 16))
+    return oda::fail(ODA_ERR_SHAPE, "rings must be 16-byte aligned");
+  if (n_sink < 0 || window < 1) return oda::fail(ODA_ERR_SHAPE, "n_sink >= 0 and window >= 1 required");
+  return run_commit(shape, k_cache, v_cache, block_table, seq_lens, k_local, v_local, k_full, v_full, flags, advance,
+                    workspace, workspace_bytes, k_ring, v_ring, n_sink, window, stream);
 }

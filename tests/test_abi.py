@@ -221,6 +221,64 @@ def test_commit_rejects_bad_arguments(L):
     assert e.value.status == -3
 
 
+def test_ring_elements(L):
+    """Direct-ring Local rings: SB = ceil(s/16) sink blocks plus RB = ceil(w/16) + 2
+    ring blocks per (layer, request, KV head), each block 16 * D elements."""
+    s = _shape(L)                                   # L=2, B=3, Hkv=2, D=128
+    per_block = 2 * 3 * 2 * 16 * 128
+    assert L.ring_elements(s, 4, 40) == (1 + 5) * per_block
+    assert L.ring_elements(s, 0, 16) == (0 + 3) * per_block
+    assert L.ring_elements(s, 20, 2048) == (2 + 130) * per_block
+    assert L.ring_elements(s, 16, 17) == (1 + 4) * per_block
+    for n_sink, window in [(-1, 16), (0, 0)]:
+        with pytest.raises(L.OdaError) as e:
+            L.ring_elements(s, n_sink, window)
+        assert e.value.status == -2
+
+
+def test_ring_calls_reject_bad_arguments(L):
+    s = _shape(L)
+    inp = L.inputs(0x1000, None, None, None, 0x4000, 0.1)
+
+    def status_of(fn):
+        with pytest.raises(L.OdaError) as e:
+            fn()
+        return e.value.status
+
+    fill = dict(kc=0x1000, vc=0x2000, t=0x3000, seq=0x4000, kr=0x5000, vr=0x6000, s=4, w=40)
+
+    def do_fill(**kw):
+        a = dict(fill)
+        a.update(kw)
+        L.ring_fill(a.get("shape", s), a["kc"], a["vc"], a["t"], a["seq"], a["s"], a["w"], a["kr"], a["vr"], stream=0)
+
+    for kw, st in [(dict(kc=None), -1), (dict(t=None), -1), (dict(kr=None), -1), (dict(vr=0x6008), -2),
+                   (dict(w=0), -2), (dict(s=-1), -2), (dict(shape=_shape(L, head_dim=96)), -3)]:
+        assert status_of(lambda: do_fill(**kw)) == st, kw
+
+    def local(inp=inp, kr=0x5000, vr=0x6000, n_sink=4, window=40, out=0x7000, shape=s):
+        L.local_decode_attn_ring(shape, inp, kr, vr, n_sink, window, out, None, None, 0, stream=0)
+
+    assert status_of(lambda: local(kr=None)) == -1
+    assert status_of(lambda: local(inp=L.inputs(None, None, None, None, 0x4000, 0.1))) == -1
+    assert status_of(lambda: local(inp=L.inputs(0x1000, None, None, None, 0x4000, 0.1, 0x8000, None))) == -1
+    assert status_of(lambda: local(out=None)) == -1
+    assert status_of(lambda: local(vr=0x6004)) == -2
+    assert status_of(lambda: local(inp=L.inputs(0x1000, None, None, None, 0x4000, 0.0))) == -2
+    assert status_of(lambda: local(window=0)) == -2
+    assert status_of(lambda: local(n_sink=-1)) == -2
+    assert status_of(lambda: local(shape=_shape(L, num_q_heads=7))) == -2
+
+    def commit(kr=0x5000, vr=0x6000, n_sink=4, window=40, kc=0x1000):
+        L.commit_kv_ring(s, kc, 0x2000, 0x3000, 0x4000, 0x9000, 0xa000, None, None, None, True, 0x8000,
+                         kr, vr, n_sink, window, workspace_bytes=256, stream=0)
+
+    assert status_of(lambda: commit(kr=None)) == -1
+    assert status_of(lambda: commit(vr=0x6002)) == -2
+    assert status_of(lambda: commit(window=0)) == -2
+    assert status_of(lambda: commit(kc=None)) == -1
+
+
 def test_decoder_entry_points_reject_bad_arguments(L):
     def status_of(fn):
         with pytest.raises(L.OdaError) as e:

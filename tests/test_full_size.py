@@ -1,8 +1,9 @@
 """Parity at the measured configurations' full sizes, in the launch
-configuration bench.py times (stacked calls, automatic work plan): one decode
-step on the GPU, then sampled (layer, request) rows recomputed by the fp64
-oracle from copies of exactly the blocks those rows read.  Gate scores and
-flags are compared for every request."""
+configuration bench.py times (stacked calls, automatic work plan, Local from
+the direct-ring workspace; the Mixed step also with Local from the paged
+cache): one decode step on the GPU, then sampled (layer, request) rows
+recomputed by the fp64 oracle from copies of exactly the blocks those rows
+read.  Gate scores and flags are compared for every request."""
 import gc
 import math
 
@@ -17,10 +18,10 @@ from oracle import gate as OG
 pytestmark = pytest.mark.gpu
 
 
-def _bench(name, head="paper"):
+def _bench(name, head="paper", local="ring"):
     import bench as BN
     from paper_2609_20734_amd import workloads as WL
-    return BN.Bench(WL.ALL[name], head, 1234, 1)
+    return BN.Bench(WL.ALL[name], head, 1234, 1, local=local)
 
 
 def _host_slice(b, st, layer, req):
@@ -124,10 +125,11 @@ def test_long_full_size():
     _check_rows(b, flags, [(0, l, r) for l in (0, 16, 31) for r in range(b.wl.batch)])
 
 
-def test_mixed_full_size():
+@pytest.mark.parametrize("local", ["ring", "paged"])
+def test_mixed_full_size(local):
     """Layers {0, L/2, L-1} x four seeded requests, plus the longest flagged
     and the shortest unflagged request."""
-    b = _bench("mixed")
+    b = _bench("mixed", local=local)
     tau = _median_tau(b)
     _run_step(b, tau)
     flags = _check_gate(b, tau)
