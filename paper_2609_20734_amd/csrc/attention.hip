@@ -53,6 +53,7 @@ constexpr int kBlock = 16;            // positions per KV block
 constexpr int kMaxGroup = 16;         // query heads per KV head held by one MFMA tile
 constexpr int kWaves = 8;             // wavefronts per split workgroup
 constexpr int kTargetGroups = 256;    // workgroups a call aims for (one per CU)
+constexpr int kBalanceBlocks = 512;   // shortest split the plan adds to even out the CUs
 constexpr int kMergeChunk = 16;       // split partials read per round trip in the merge
 constexpr int kMergeSmall = 4;        // chunk used for the last few splits
 constexpr float kLog2e = 1.4426950408889634f;
@@ -80,8 +81,10 @@ struct AttnArgs {
   int32_t L, B, Hq, Hkv, G, MB;
   int32_t n_sink, window;   // window <= 0: no window
   int32_t has_cur;
-  int32_t bps, max_splits;  // bps: blocks per split when fixed by the caller
+  int32_t bps, max_splits;  // bps: blocks per split when fixed by the caller; max_splits:
+                            // partial slots per unit (the most splits any selection gets)
   int32_t dyn_splits;       // 1: blocks per split chosen on the device (effective_bps)
+  int32_t split_cap;        // most splits per unit the automatic plan considers
   int32_t nvb_max;          // host bound on visited blocks per request
   int32_t lpi;              // layers per work item (attn_local_layers_kernel)
   int32_t select;
@@ -212,17 +215,54 @@ __device__ __forceinline__ bool request_of_rank(const AttnArgs& a, int rank, int
   return false;
 }
 
-// Blocks per split for this call.  With the automatic plan the split count
-// depends on how many requests are selected (known only on the device for
-// Full): enough splits that the selected requests give about
-// kTargetGroups workgroups, at most max_splits (sized for one request).
+// Splits per unit for `units` units, at least `want` and at most `cap`.  A CU
+// streams at only ~34 GB/s (about 1/200 of HBM's rate), whether it holds one
+// workgroup or two, so a launch whose CUs do not all hold the same number of
+// equal workgroups runs at the pace of those holding one more: 96 units in 3
+// splits (288 workgroups on 256 CUs) read at 4.9 TB/s, in 5 splits (480) at
+// 6.3.  For m = 1, 2, ... workgroups
+// per CU the largest count s >= want with units * s <= 256 m is taken as soon
+// as it fills the CUs within 10% of evenly; if no count up to `cap` does, the
+// most even one.  A dozen steps at most, the same on the host (plan) and on
+// the device (selected requests).
+__host__ __device__ __forceinline__ int64_t balanced_splits(int64_t units, int64_t want, int64_t cap) {
+  if (want >= cap) return cap;
+  int64_t best = want;
+  int64_t best_m = (units * want + kTargetGroups - 1) / kTargetGroups;   // workgroups per CU at `want`
+  for (int64_t m = best_m; m <= best_m + 16; ++m) {
+    const int64_t s = kTargetGroups * m / units;
+    if (s > cap) break;
+    if (kTargetGroups * m * 10 <= units * s * 11) return s;
+    if (m * best < best_m * s) {   // m / s below best_m / best: more even
+      best = s;
+      best_m = m;
+    }
+  }
+  return best;
+}
+
+// Blocks per split of the automatic plan for `units` units (the selected
+// requests' layers and KV heads) of at most nvb_max blocks each, with at most
+// `cap` splits per unit: enough splits for about one workgroup per CU, then
+// more to even the CUs out while every split keeps kBalanceBlocks blocks.
+// Each split past the first costs its workgroup a partial write, a ticket and
+// a share of the merge: at even load, splits of 514 / 258 / 130 blocks took
+// 3.6% / 7.6% / 25% longer than whole units.
+__host__ __device__ __forceinline__ int plan_bps(int64_t units, int nvb_max, int cap) {
+  const int64_t want = (kTargetGroups + units - 1) / units;
+  int64_t s = want < cap ? want : cap;
+  const int64_t keep = nvb_max / kBalanceBlocks;   // splits that keep kBalanceBlocks blocks each
+  if (keep > s) s = balanced_splits(units, s, keep < cap ? keep : cap);
+  if (s < 1) s = 1;
+  const int bps = (int)(((nvb_max + s - 1) / s + 1) & ~(int64_t)1);
+  return bps > 2 ? bps : 2;
+}
+
+// Blocks per split for this call: fixed by the caller, or the automatic plan
+// for the number of selected requests (known only on the device for Full).
 __device__ __forceinline__ int effective_bps(const AttnArgs& a, int active) {
   if (!a.dyn_splits) return a.bps;
-  const int64_t units = (int64_t)max(active, 1) * a.L * a.Hkv;
-  const int64_t want = (kTargetGroups + units - 1) / units;
-  const int s = (int)max((int64_t)1, min((int64_t)a.max_splits, want));
-  const int bps = ((a.nvb_max + s - 1) / s + 1) & ~1;
-  return uniform(max(bps, 2));
+  return uniform(plan_bps((int64_t)max(active, 1) * a.L * a.Hkv, a.nvb_max, a.split_cap));
 }
 
 __device__ __forceinline__ bf16x8 load16(const uint16_t* p) {
@@ -699,7 +739,10 @@ void attn_split_kernel(AttnArgs a) {
   const int l = (int)(item % a.L);
   item /= a.L;
   const int rank = (int)(item % active);
-  if (item / active >= a.max_splits) return;
+  const int bps = effective_bps(a, active);
+  // no selected request has this split (the grid covers the selection with
+  // the most); the plan keeps every split below max_splits, checked anyway
+  if ((item / active) * bps >= max(a.nvb_max, 1) || item / active >= a.max_splits) return;
   const int split = (int)(item / active);
   int b;
   if (!request_of_rank(a, rank, b)) return;
@@ -732,7 +775,6 @@ void attn_split_kernel(AttnArgs a) {
   }
   Run r;
   r.geo = geometry(n, kLocal ? a.n_sink : 0, a.window, a.has_cur);
-  const int bps = effective_bps(a, active);
   // (nvb = 0 happens only with the candidate as the sole position: one item, no blocks)
   const int nsplit = max(1, (r.geo.nvb + bps - 1) / bps);
   if (split >= nsplit) return;   // uniform over the workgroup: no barrier is skipped by part of it
@@ -824,8 +866,11 @@ void attn_local_layers_kernel(AttnArgs a) {
 
 struct Plan {
   int nvb_max;
-  int bps;
-  int max_splits;
+  int bps;            // blocks per split: fixed, or the automatic plan's for all B requests
+  int max_splits;     // partial slots per unit: the most splits any selection gets
+  int split_cap;      // most splits per unit the automatic plan considers
+  int local_splits;   // splits per unit of a Local call (all B requests selected)
+  int64_t full_slots; // (request rank, split) pairs a Full grid covers: the most over selections
   int dyn;
   size_t off_o;
   size_t off_ml;
@@ -861,15 +906,17 @@ oda_status check_shape(const oda_attn_shape* s) {
 
 // Work decomposition.  One workgroup per (request, layer, KV head, split).
 // The automatic plan splits a request only as much as needed for the selected
-// requests to give the GPU about kTargetGroups workgroups (one per CU).
-// Local selects every request; Full's grid and workspace are sized for the
-// case of a single selected request (max_splits), and the kernels pick the
-// actual split count on the device (effective_bps).  The workspace size a
-// caller queries is the single-request one, which covers both.  A request
-// covered by one split is finalised by its workgroup; otherwise the last of
-// its splits merges them in the same launch.
+// requests to give the GPU about kTargetGroups workgroups (one per CU), and
+// then to a count whose workgroups spread evenly over the CUs
+// (balanced_splits).  Local selects every request; Full selects k of them,
+// known only on the device, which picks the split count for its k
+// (effective_bps).  The partial slots and the Full grid are sized for the
+// selection that needs the most, so the workspace size a caller queries
+// covers every call of the shape.  A request covered by one split is
+// finalised by its workgroup; otherwise the last of its splits merges them in
+// the same launch.
 // Workspace: the ticket words (one per unit), then the partial o, then (m, l).
-void make_plan(const oda_attn_shape* s, int n_sink, int window, int64_t selected, Plan* p) {
+void make_plan(const oda_attn_shape* s, int n_sink, int window, Plan* p) {
   const int64_t total_blocks = oda::ceil_div(s->max_seq_len, kBlock);
   int64_t nvb = total_blocks;
   if (window > 0) {
@@ -877,26 +924,41 @@ void make_plan(const oda_attn_shape* s, int n_sink, int window, int64_t selected
     nvb = std::min<int64_t>(total_blocks, sink_blocks + oda::ceil_div(window, kBlock) + 1);
   }
   const int64_t units = (int64_t)s->num_layers * s->batch * s->num_kv_heads;
-  const int64_t units_selected = (int64_t)s->num_layers * s->num_kv_heads * selected;
-  int64_t bps = s->split_blocks;
-  p->dyn = 0;
-  if (bps == 0) {
-    const int64_t want = oda::ceil_div(kTargetGroups, units_selected);
+  const int64_t per_request = (int64_t)s->num_layers * s->num_kv_heads;
+  p->nvb_max = (int)nvb;
+  p->split_cap = 1;
+  if (s->split_blocks != 0) {
+    p->dyn = 0;
+    p->bps = s->split_blocks;
+    p->max_splits = (int)oda::ceil_div(nvb, s->split_blocks);
+    p->local_splits = p->max_splits;
+    p->full_slots = (int64_t)s->batch * p->max_splits;
+  } else {
     // at least kWaves blocks (four block pairs) per split: a small call gets
     // more, shorter splits, which shortens the split phase more than the merge
     // of more partials costs (half of a split's wavefronts may be idle).  More
     // than kMergeChunk splits add a round trip to the merge, so they are taken
     // only while each split still has 8 * kWaves blocks (four pairs per
     // wavefront)
-    const int64_t max_split =
-        std::max<int64_t>(1, std::min<int64_t>(nvb / kWaves, std::max<int64_t>(kMergeChunk, nvb / (8 * kWaves))));
-    const int64_t nsplit = std::max<int64_t>(1, std::min(want, max_split));
-    bps = oda::round_up(oda::ceil_div(nvb, nsplit), 2);
     p->dyn = 1;
+    p->split_cap = (int)std::max<int64_t>(
+        1, std::min<int64_t>(nvb / kWaves, std::max<int64_t>(kMergeChunk, nvb / (8 * kWaves))));
+    // the device picks the split count for the number k of selected requests
+    // (plan_bps); a Local call selects all B.  Partial slots and the Full grid
+    // cover every k: from 10 CUs' worth of units on, one split per unit is
+    // already even, so larger k add k requests of one split each.
+    const int64_t k_even = oda::ceil_div(10 * kTargetGroups, per_request);
+    p->max_splits = 1;
+    p->full_slots = s->batch;
+    for (int64_t k = 1; k <= std::min<int64_t>(s->batch, k_even); ++k) {
+      const int bps = plan_bps(k * per_request, (int)nvb, p->split_cap);
+      const int64_t ns = oda::ceil_div(nvb, bps);
+      p->max_splits = (int)std::max<int64_t>(p->max_splits, ns);
+      p->full_slots = std::max<int64_t>(p->full_slots, k * ns);
+    }
+    p->bps = plan_bps(s->batch * per_request, (int)nvb, p->split_cap);
+    p->local_splits = (int)oda::ceil_div(nvb, p->bps);
   }
-  p->nvb_max = (int)nvb;
-  p->bps = (int)std::min<int64_t>(bps, 1 << 30);
-  p->max_splits = (int)oda::ceil_div(nvb, bps);
   if (p->max_splits <= 1) {
     p->off_o = 0;
     p->off_ml = 0;
@@ -949,7 +1011,7 @@ oda_status check_inputs(const oda_attn_inputs* in, const float* out, const oda_a
 // leave at least kTargetGroups workgroups, when every unit has one split;
 // 1 (the split kernel) otherwise.
 int layers_per_item(const oda_attn_shape* s, const Plan& plan) {
-  if (plan.max_splits != 1) return 1;
+  if (plan.local_splits != 1) return 1;
   const int64_t per_layer = (int64_t)s->batch * s->num_kv_heads;
   for (int d = s->num_layers; d > 1; --d)
     if (s->num_layers % d == 0 && (s->num_layers / d) * per_layer >= kTargetGroups) return d;
@@ -988,8 +1050,7 @@ oda_status launch_layers(const AttnArgs& args, hipStream_t stream) {
 template <int D, bool kLocal>
 oda_status launch(const AttnArgs& args, const Plan& plan, hipStream_t stream) {
   if (kLocal && args.lpi > 1) return launch_layers<D>(args, stream);
-  const int64_t units = (int64_t)args.L * args.B * args.Hkv;
-  const int64_t items = units * plan.max_splits;
+  const int64_t items = (int64_t)args.L * args.Hkv * (kLocal ? (int64_t)args.B * plan.local_splits : plan.full_slots);
   if (items > 0x7fffffffLL) return oda::fail(ODA_ERR_SHAPE, "grid too large (%lld work items)", (long long)items);
   const size_t lds = split_lds_floats(args.G, D) * sizeof(float) + (args.qkv ? prep_lds_bytes(args.G, D) : 0);
   static std::atomic<uint64_t> lds_raised{0};
@@ -1009,7 +1070,7 @@ oda_status run_attention(const oda_attn_shape* s, const oda_attn_inputs* in, boo
                          const uint16_t* v_ring = nullptr) {
   Plan plan;
   // Local attends every request; Full is sized for the fewest selected (one)
-  make_plan(s, n_sink, window, local ? s->batch : 1, &plan);
+  make_plan(s, n_sink, window, &plan);
   if (plan.bytes > 0) {
     if (ws == nullptr) return oda::fail(ODA_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", plan.bytes);
     if (ws_bytes < plan.bytes)
@@ -1059,6 +1120,7 @@ oda_status run_attention(const oda_attn_shape* s, const oda_attn_inputs* in, boo
   a.bps = plan.bps;
   a.max_splits = plan.max_splits;
   a.dyn_splits = plan.dyn;
+  a.split_cap = plan.split_cap;
   a.nvb_max = plan.nvb_max;
   a.lpi = local ? layers_per_item(s, plan) : 1;
   a.select = select;
@@ -1081,7 +1143,7 @@ extern "C" oda_status oda_attn_workspace_size(const oda_attn_shape* shape, int32
   if (bytes == nullptr) return oda::fail(ODA_ERR_NULL, "bytes is NULL");
   if (n_sink < 0 || window < 0) return oda::fail(ODA_ERR_SHAPE, "n_sink and window must be >= 0");
   Plan plan;
-  make_plan(shape, n_sink, window, 1, &plan);   // covers Local and Full calls of this shape
+  make_plan(shape, n_sink, window, &plan);   // covers Local and Full calls of this shape
   *bytes = plan.bytes;
   return oda::ok();
 }

@@ -159,6 +159,24 @@ def test_hybrid_full_size():
     _check_rows(b, flags, rows)
 
 
+def test_hybrid_full_size_one_request_flagged():
+    """One request flagged by a prescribed schedule: the gated layers' Full
+    launch covers the request's 96 (layer, KV head) units in 5 splits each
+    (480 workgroups, about two per CU) merged in the launch, the natively
+    windowed layers' in one split each."""
+    b = _bench("hybrid")
+    B = b.wl.batch
+    forced = torch.zeros((1, B), dtype=torch.int32, device="cuda")
+    forced[0, 5] = 1
+    for c in b.step_calls(math.inf, forced)[0]:
+        c()
+    torch.cuda.synchronize()
+    flags = b.flags.cpu().numpy().astype(bool)
+    assert flags.tolist() == [r == 5 for r in range(B)]
+    assert int(b.n_work.item()) == 1 and int(b.work[0].item()) == 5
+    _check_rows(b, flags, [(1, 0, 5), (1, 6, 5), (1, 11, 5), (0, 0, 5), (0, 35, 5), (1, 4, 2), (0, 17, 7)])
+
+
 def test_llama_per_layer_launches_eager_and_graph():
     """The per-layer launch mode (one call per layer, the gate reading staged
     inputs): parity with the oracle, and a captured graph of it replays to the
