@@ -54,6 +54,7 @@ constexpr int kMaxGroup = 16;         // query heads per KV head held by one MFM
 constexpr int kWaves = 8;             // wavefronts per split workgroup
 constexpr int kTargetGroups = 256;    // workgroups a call aims for (one per CU)
 constexpr int kBalanceBlocks = 512;   // shortest split the plan adds to even out the CUs
+constexpr int kBalanceUnits = 64;     // units per request from which the plan evens out the CUs
 constexpr int kMergeChunk = 16;       // split partials read per round trip in the merge
 constexpr int kMergeSmall = 4;        // chunk used for the last few splits
 constexpr float kLog2e = 1.4426950408889634f;
@@ -242,17 +243,21 @@ __host__ __device__ __forceinline__ int64_t balanced_splits(int64_t units, int64
 }
 
 // Blocks per split of the automatic plan for `units` units (the selected
-// requests' layers and KV heads) of at most nvb_max blocks each, with at most
-// `cap` splits per unit: enough splits for about one workgroup per CU, then
-// more to even the CUs out while every split keeps kBalanceBlocks blocks.
-// Each split past the first costs its workgroup a partial write, a ticket and
-// a share of the merge: at even load, splits of 514 / 258 / 130 blocks took
-// 3.6% / 7.6% / 25% longer than whole units.
-__host__ __device__ __forceinline__ int plan_bps(int64_t units, int nvb_max, int cap) {
+// requests' layers and KV heads, `per_request` of them per request) of at
+// most nvb_max blocks each, with at most `cap` splits per unit: enough splits
+// for about one workgroup per CU, then more to even the CUs out while every
+// split keeps kBalanceBlocks blocks.  Each split past the first costs its
+// workgroup a partial write, a ticket and a share of the merge: at even load,
+// splits of 514 / 258 / 130 blocks took 3.6% / 7.6% / 25% longer than whole
+// units.  The evening assumes units of equal length, which holds for the
+// units of one request; when a request has fewer than kBalanceUnits of them
+// (one-layer calls), the spread of the requests' lengths sets the balance
+// instead, and more splits made per-layer calls over 8K-64K requests slower.
+__host__ __device__ __forceinline__ int plan_bps(int64_t units, int64_t per_request, int nvb_max, int cap) {
   const int64_t want = (kTargetGroups + units - 1) / units;
   int64_t s = want < cap ? want : cap;
   const int64_t keep = nvb_max / kBalanceBlocks;   // splits that keep kBalanceBlocks blocks each
-  if (keep > s) s = balanced_splits(units, s, keep < cap ? keep : cap);
+  if (per_request >= kBalanceUnits && keep > s) s = balanced_splits(units, s, keep < cap ? keep : cap);
   if (s < 1) s = 1;
   const int bps = (int)(((nvb_max + s - 1) / s + 1) & ~(int64_t)1);
   return bps > 2 ? bps : 2;
@@ -262,7 +267,7 @@ __host__ __device__ __forceinline__ int plan_bps(int64_t units, int nvb_max, int
 // for the number of selected requests (known only on the device for Full).
 __device__ __forceinline__ int effective_bps(const AttnArgs& a, int active) {
   if (!a.dyn_splits) return a.bps;
-  return uniform(plan_bps((int64_t)max(active, 1) * a.L * a.Hkv, a.nvb_max, a.split_cap));
+  return uniform(plan_bps((int64_t)max(active, 1) * a.L * a.Hkv, (int64_t)a.L * a.Hkv, a.nvb_max, a.split_cap));
 }
 
 __device__ __forceinline__ bf16x8 load16(const uint16_t* p) {
@@ -951,12 +956,12 @@ void make_plan(const oda_attn_shape* s, int n_sink, int window, Plan* p) {
     p->max_splits = 1;
     p->full_slots = s->batch;
     for (int64_t k = 1; k <= std::min<int64_t>(s->batch, k_even); ++k) {
-      const int bps = plan_bps(k * per_request, (int)nvb, p->split_cap);
+      const int bps = plan_bps(k * per_request, per_request, (int)nvb, p->split_cap);
       const int64_t ns = oda::ceil_div(nvb, bps);
       p->max_splits = (int)std::max<int64_t>(p->max_splits, ns);
       p->full_slots = std::max<int64_t>(p->full_slots, k * ns);
     }
-    p->bps = plan_bps(s->batch * per_request, (int)nvb, p->split_cap);
+    p->bps = plan_bps(s->batch * per_request, per_request, (int)nvb, p->split_cap);
     p->local_splits = (int)oda::ceil_div(nvb, p->bps);
   }
   if (p->max_splits <= 1) {
