@@ -17,6 +17,13 @@ if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_20734_amd.build` "
                       "(or __graft_entry__.build()) before using the HIP path")
 
+# torch's wheel carries its own HIP and HSA runtimes.  Importing torch before
+# the library makes the dynamic loader resolve the library's libamdhip64
+# against torch's copy, so the process holds one runtime.  Loaded first, the
+# library would map the system's runtime beside torch's, and whichever of the
+# two HSA runtimes starts second finds no GPU ("no ROCm-capable device").
+import torch  # noqa: E402,F401  (load order; the tensors come from torch anyway)
+
 _lib = ctypes.CDLL(LIB_PATH)
 
 ODA_OK = 0

@@ -5,6 +5,8 @@ import ctypes
 import math
 import os
 import re
+import subprocess
+import sys
 
 import pytest
 
@@ -337,3 +339,15 @@ def test_stream_read_rejects_bad_arguments(L):
     assert status_of_read(nbytes=4100) == -2                  # not a multiple of 16
     assert status_of_read(groups=-1) == -2
     L.stream_read(0x10000, 0, 0x20000, 0, stream=0)           # nothing to read: no launch
+
+
+def test_library_shares_torchs_hip_runtime():
+    """Importing the binding before anything else still leaves one HIP
+    runtime in the process (torch's): a second one would find no GPU."""
+    code = ("import paper_2609_20734_amd._lib, torch\n"
+            "maps = open('/proc/self/maps').read()\n"
+            "libs = {l.split()[-1] for l in maps.splitlines() if 'libamdhip64' in l}\n"
+            "print(len(libs), sorted(libs))\n")
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300, cwd=ROOT)
+    assert r.returncode == 0, r.stderr[-2000:]
+    assert r.stdout.startswith("1 "), r.stdout
