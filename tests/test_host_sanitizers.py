@@ -36,6 +36,20 @@ def build_sanitized(out):
     return out
 
 
+def sanitized_tree(tmp_path, lib):
+    """A copy of the package (the sanitized build as its liboda.so), the
+    header and the ABI tests, so the tests load the instrumented library."""
+    tree = tmp_path / "tree"
+    shutil.copytree(os.path.join(ROOT, "paper_2609_20734_amd"), tree / "paper_2609_20734_amd",
+                    ignore=shutil.ignore_patterns("__pycache__", "*.so", "*.so.tmp"))
+    shutil.copy(lib, tree / "paper_2609_20734_amd" / "liboda.so")
+    shutil.copytree(os.path.join(ROOT, "include"), tree / "include")
+    (tree / "tests").mkdir()
+    for f in ("conftest.py", "test_abi.py"):
+        shutil.copy(os.path.join(ROOT, "tests", f), tree / "tests" / f)
+    return tree
+
+
 def test_abi_checks_pass_under_host_sanitizers(tmp_path):
     rt = asan_runtime()
     if rt is None:
@@ -44,13 +58,18 @@ def test_abi_checks_pass_under_host_sanitizers(tmp_path):
     # the instrumented library needs the sanitizer runtime, i.e. the build took effect
     dyn = subprocess.run(["readelf", "-d", lib], capture_output=True, text=True).stdout
     assert "libclang_rt.asan" in dyn, dyn
+    tree = sanitized_tree(tmp_path, lib)
     env = dict(os.environ)
-    env.update(ODA_LIBRARY=lib, LD_PRELOAD=rt,
-               LD_LIBRARY_PATH=os.path.dirname(rt) + os.pathsep + env.get("LD_LIBRARY_PATH", ""),
+    env.update(LD_PRELOAD=rt, LD_LIBRARY_PATH=os.path.dirname(rt) + os.pathsep + env.get("LD_LIBRARY_PATH", ""),
                ASAN_OPTIONS="detect_leaks=0", UBSAN_OPTIONS="print_stacktrace=1:halt_on_error=1")
+    # the child reports which library it loaded: the instrumented copy, not the in-tree build
+    probe = subprocess.run([sys.executable, "-c", "import paper_2609_20734_amd._lib as L; print(L.LIB_PATH)"],
+                           env=env, capture_output=True, text=True, timeout=300, cwd=str(tree))
+    assert probe.returncode == 0, probe.stderr[-3000:]
+    assert probe.stdout.strip() == str(tree / "paper_2609_20734_amd" / "liboda.so"), probe.stdout
     res = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                          os.path.join(ROOT, "tests", "test_abi.py")],
-                         env=env, capture_output=True, text=True, timeout=600, cwd=ROOT)
+                          str(tree / "tests" / "test_abi.py")],
+                         env=env, capture_output=True, text=True, timeout=600, cwd=str(tree))
     out = res.stdout + res.stderr
     assert res.returncode == 0, out[-4000:]
     assert "AddressSanitizer" not in out and "runtime error" not in out, out[-4000:]
