@@ -216,12 +216,12 @@ __device__ __forceinline__ bool request_of_rank(const AttnArgs& a, int rank, int
   return false;
 }
 
-// Splits per unit for `units` units, at least `want` and at most `cap`.  A CU
-// streams at only ~34 GB/s (about 1/200 of HBM's rate), whether it holds one
-// workgroup or two, so a launch whose CUs do not all hold the same number of
-// equal workgroups runs at the pace of those holding one more: 96 units in 3
-// splits (288 workgroups on 256 CUs) read at 4.9 TB/s, in 5 splits (480) at
-// 6.3.  For m = 1, 2, ... workgroups per CU the largest count s >= want with
+// Splits per unit for `units` units, at least `want` and at most `cap`.  While
+// a launch keeps HBM busy, a CU streams at only ~27-34 GB/s (about 1/200 of
+// HBM's rate) whether it holds one workgroup or two (alone, ~55), so a launch
+// whose CUs do not all hold the same number of equal workgroups runs at the
+// pace of those holding one more: 96 units in 3 splits (288 workgroups on 256
+// CUs) read at 4.9 TB/s, in 5 splits (480) at 6.3.  For m = 1, 2, ... workgroups per CU the largest count s >= want with
 // units * s <= 256 m is taken as soon as it fills the CUs within 10% of
 // evenly; if no count up to `cap` does, the most even one.  At most 17 steps,
 // the same on the host (plan) and on the device (selected requests).
