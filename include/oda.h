@@ -124,8 +124,9 @@ typedef struct {
 
 /* Bytes of workspace an attention call with this shape and access set needs
  * (one merge-ticket word per (layer, request, KV head), then the split-K
- * partials).  It is 0 when every request fits one work item; the workspace
- * pointer may then be NULL.  window == 0 means "no window" (the whole
+ * partials), whatever number of requests a Full call selects: the split
+ * count depends on that number and the size covers the largest.  It is 0 when
+ * every request fits one work item; the workspace pointer may then be NULL.  window == 0 means "no window" (the whole
  * history); window > 0 limits the recent part to `window` positions.
  * n_sink >= 0.  (host out)
  * A workspace must be zero-filled before its first use (e.g. allocated
