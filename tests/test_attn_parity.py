@@ -313,6 +313,34 @@ def test_selection_sizes_on_one_workspace(cur):
                 assert np.all(o[:, b] == -7.0) and np.all(ls[:, b] == -7.0)
 
 
+def test_selection_sizes_with_balanced_splits():
+    """96 (layer, KV head) units per request (12 layers x 8 KV heads) and a
+    41,000-position history (2,563 blocks): Full over 1, 2, 3 and 4 selected
+    requests takes 5, 4, 5 and 2 splits per unit, the counts that spread the
+    workgroups evenly over the CUs, and merges them in the launch; the shorter
+    requests get fewer splits.  Every selection on one workspace matches the
+    oracle, leaves the unselected rows untouched and the ticket words zero."""
+    seq = [41000, 3000, 1, 5000]
+    pb = AttnProblem(97, 12, 4, 32, 8, 64, seq, cur=True)
+    P = pb.P
+    ws = torch.zeros(max(256, P.attn_workspace_size(pb.shape, 0, 0)), dtype=torch.uint8, device="cuda")
+    units = pb.L * pb.B * pb.Hkv
+    ref_o, ref_l, _ = pb.oracle_full(0, requests=[0, 1, 2, 3])
+    for sel in ([0], [3, 0], [1, 0, 3], [2, 0, 3, 1]):
+        out, lse = pb.new_out(-7.0)
+        wl = np.zeros(4, np.int32)
+        wl[:len(sel)] = sel
+        P.full_decode_attn(pb.shape, pb.inp, 0, None, dev_i32(wl), dev_i32([len(sel)]), out, lse, ws)
+        torch.cuda.synchronize()
+        assert int(ws[:4 * units].view(torch.int32).abs().sum().item()) == 0, sel
+        o, ls = out.cpu().numpy(), lse.cpu().numpy()
+        for b in sel:
+            check_close(o[:, b], ref_o[:, b], what=f"selection {sel} request {b}")
+            assert np.max(np.abs(ls[:, b] - ref_l[:, b])) <= LSE_ABS
+        for b in set(range(4)) - set(sel):
+            assert np.all(o[:, b] == -7.0) and np.all(ls[:, b] == -7.0)
+
+
 @pytest.mark.parametrize("cur,walk", [(False, False), (True, False), (True, True)])
 def test_layer_stride_between_layers(cur, walk):
     """layer_stride_kv: each layer's blocks start `stride` elements after the
