@@ -347,7 +347,8 @@ def test_layer_stride_between_layers(cur, walk):
     previous layer's (here the dense size plus padding, as in one allocation
     holding several layer groups).  Local and Full read the right layers and
     match the oracle on the dense copies; `walk` takes a batch large enough
-    that Local's workgroups each walk all four layers of a (request, KV head)."""
+    that Local's workgroups each walk all four layers of a (request, KV head).
+    Rings filled from the padded caches give Local the same bits."""
     if walk:
         seq = np.random.default_rng(58).integers(1, 300, size=64).tolist()
         pb = AttnProblem(58, 4, 64, 8, 8, 64, seq, cur=cur)
@@ -376,3 +377,15 @@ def test_layer_stride_between_layers(cur, walk):
             want = pb.oracle_full(0)
         torch.cuda.synchronize()
         _cmp(pb, (out, lse), want)
+        if local:
+            # rings filled from the padded layers give the same bits as the paged Local
+            n = P.ring_elements(shape, 4, 64)
+            kr = torch.full((n,), 0x7FC0, dtype=torch.int16, device="cuda")
+            vr = torch.full((n,), 0x7FC0, dtype=torch.int16, device="cuda")
+            P.ring_fill(shape, k_pad, v_pad, pb.dtable, pb.dseq, 4, 64, kr, vr)
+            out_r, lse_r = pb.new_out(np.nan)
+            P.local_decode_attn_ring(shape, P.inputs(pb.dq, None, None, None, pb.dseq, pb.scale, pb.dkc, pb.dvc),
+                                     kr, vr, 4, 64, out_r, lse_r, ws)
+            torch.cuda.synchronize()
+            assert torch.equal(out_r.view(torch.int32), out.view(torch.int32))
+            assert torch.equal(lse_r.view(torch.int32), lse.view(torch.int32))
