@@ -1,7 +1,9 @@
 """Seeded random selected-state commits (App. A.5 commit equation) against
 the oracle's commit: layer count, batch, KV heads, head width, lengths
 (block boundaries included), per-request flags, with and without the Full
-candidates, the length advance on or off, dense or padded layer strides."""
+candidates, the length advance on or off, dense or padded layer strides;
+half the cases also keep direct-ring Local rings current, checked by a Local
+call at the new lengths against the paged one (bit for bit)."""
 import numpy as np
 import pytest
 import torch
@@ -25,7 +27,7 @@ def test_random_commits(seed):
     with_full = bool(g.random() < 0.7)
     advance = bool(g.random() < 0.8)
     flags = (g.random(B) < 0.5).astype(np.int32)
-    mb = int(np.ceil(seq.max() / 16))
+    mb = int(np.ceil((seq.max() + 1) / 16))   # room for a Local call at the advanced lengths
     table, nb = S.paged_block_table(S.rng(6000 + seed, S.STREAM_TABLE), seq, mb, permute=True, extra_blocks=2)
     k, v = S.kv_cache(6000 + seed, L, nb, Hkv, D)
     kl = S.normal_bf16(S.rng(6100 + seed, S.STREAM_KCUR), (L, B, Hkv, D))
@@ -43,11 +45,22 @@ def test_random_commits(seed):
     else:
         dk, dv = dev_u16(k), dev_u16(v)
     dseq = dev_i32(seq)
+    dtable = dev_i32(table)
     shape = P.Shape(L, B, Hkv, Hkv, D, mb, int(seq.max()), nb, layer_stride_kv=stride)
     ws = torch.zeros(P.commit_workspace_size(shape), dtype=torch.uint8, device="cuda")
-    P.commit_kv(shape, dk, dv, dev_i32(table), dseq, dev_u16(kl), dev_u16(vl),
-                dev_u16(kf) if with_full else None, dev_u16(vf) if with_full else None,
-                dev_i32(flags) if with_full else None, advance, ws)
+    # half the cases commit into direct-ring Local rings too (filled at the pre-commit lengths)
+    ring = bool(g.random() < 0.5)
+    n_sink, window = int(g.choice([0, 4, 20])), int(g.integers(16, 200))
+    args = (shape, dk, dv, dtable, dseq, dev_u16(kl), dev_u16(vl), dev_u16(kf) if with_full else None,
+            dev_u16(vf) if with_full else None, dev_i32(flags) if with_full else None, advance, ws)
+    if ring:
+        n = P.ring_elements(shape, n_sink, window)
+        kr = torch.full((n,), 0x7FC0, dtype=torch.int16, device="cuda")
+        vr = torch.full((n,), 0x7FC0, dtype=torch.int16, device="cuda")
+        P.ring_fill(shape, dk, dv, dtable, dseq, n_sink, window, kr, vr)
+        P.commit_kv_ring(*args, k_ring=kr, v_ring=vr, n_sink=n_sink, window=window)
+    else:
+        P.commit_kv(*args)
     torch.cuda.synchronize()
     hk, hv, hseq = k.copy(), v.copy(), seq.copy()
     sel = flags if with_full else np.zeros(B, np.int32)
@@ -62,3 +75,25 @@ def test_random_commits(seed):
     assert np.array_equal(gv.view(np.uint16), hv)
     assert dseq.cpu().numpy().tolist() == (hseq if advance else seq).tolist()
     assert int(ws.sum().item()) == 0      # the tickets are back at zero
+    if ring:
+        # Local at the new lengths with a fresh candidate: the rings, kept current
+        # by the commit, give the paged call's bits
+        q = dev_u16(S.normal_bf16(S.rng(6300 + seed, S.STREAM_Q), (L, B, Hkv, D)))
+        kc = dev_u16(S.normal_bf16(S.rng(6400 + seed, S.STREAM_KCUR), (L, B, Hkv, D)))
+        vc = dev_u16(S.normal_bf16(S.rng(6400 + seed, S.STREAM_VCUR), (L, B, Hkv, D)))
+        lshape = P.Shape(L, B, Hkv, Hkv, D, mb, int(seq.max()) + 1, nb, layer_stride_kv=stride)
+        wsl = torch.zeros(max(256, P.attn_workspace_size(lshape, n_sink, window)), dtype=torch.uint8, device="cuda")
+        outs = []
+        for use_ring in (False, True):
+            out = torch.full((L, B, Hkv, D), float("nan"), device="cuda")
+            lse = torch.full((L, B, Hkv), float("nan"), device="cuda")
+            if use_ring:
+                P.local_decode_attn_ring(lshape, P.inputs(q, None, None, None, dseq, D ** -0.5, kc, vc), kr, vr,
+                                         n_sink, window, out, lse, wsl)
+            else:
+                P.local_decode_attn(lshape, P.inputs(q, dk, dv, dtable, dseq, D ** -0.5, kc, vc), n_sink, window,
+                                    out, lse, wsl)
+            torch.cuda.synchronize()
+            outs.append((out, lse))
+        assert torch.equal(outs[0][0].view(torch.int32), outs[1][0].view(torch.int32))
+        assert torch.equal(outs[0][1].view(torch.int32), outs[1][1].view(torch.int32))
