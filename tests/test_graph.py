@@ -5,7 +5,8 @@ period (its own attention, selection and commit on host copies).  Replays are
 separated by eager work and host synchronisation, and every replay is checked:
 each step's outputs against the oracle within the attention bar, and outputs,
 final caches, lengths and recall counter bit-identical to the eager run (the
-caches and lengths also equal the oracle's bit for bit)."""
+caches and lengths also equal the oracle's bit for bit).  One case reads
+Local from direct-ring rings that the captured commits keep current."""
 import math
 
 import numpy as np
@@ -20,8 +21,8 @@ from oracle import step as OS
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("dt", [16, 64])      # two tower widths
-def test_graph_replay_matches_eager(dt):
+@pytest.mark.parametrize("dt,local", [(16, "paged"), (64, "paged"), (16, "ring")])   # two tower widths; Local
+def test_graph_replay_matches_eager(dt, local):                                      # from the cache or the rings
     P = need_gpu()
     L, B, Hkv, G, D, T = 2, 3, 2, 4, 128, 8
     Hq = Hkv * G
@@ -58,19 +59,35 @@ def test_graph_replay_matches_eager(dt):
     lses = torch.zeros(T, L, B, Hq, device="cuda")
     scale = 1.0 / math.sqrt(D)
 
+    ring = local == "ring"
+    if ring:   # direct-ring Local: rings refilled from the cache at every reset, kept current by the commit
+        n_ring = P.ring_elements(shape, s, W)
+        kr = torch.full((n_ring,), 0x7FC0, dtype=torch.int16, device="cuda")
+        vr = torch.full((n_ring,), 0x7FC0, dtype=torch.int16, device="cuda")
+
     def period():
         for t in range(T):
-            P.local_decode_attn(shape, P.inputs(q[t], dk, dv, dtab, dseq, scale, kl[t], vl[t]), s, W, outs[t],
-                                lses[t], ws_l)
+            if ring:
+                P.local_decode_attn_ring(shape, P.inputs(q[t], None, None, None, dseq, scale, kl[t], vl[t]), kr, vr,
+                                         s, W, outs[t], lses[t], ws_l)
+            else:
+                P.local_decode_attn(shape, P.inputs(q[t], dk, dv, dtab, dseq, scale, kl[t], vl[t]), s, W, outs[t],
+                                    lses[t], ws_l)
             P.recall_gate(gate, B, h[t], e[t], hl[t], 0.0, forced[t], score, flags, wl, nw, ctr, ws_g)
             P.full_decode_attn(shape, P.inputs(q[t], dk, dv, dtab, dseq, scale, kf[t], vf[t]), 0, None, wl, nw,
                                outs[t], lses[t], ws_f)
-            P.commit_kv(shape, dk, dv, dtab, dseq, kl[t], vl[t], kf[t], vf[t], flags, True, ws_c)
+            if ring:
+                P.commit_kv_ring(shape, dk, dv, dtab, dseq, kl[t], vl[t], kf[t], vf[t], flags, True, ws_c,
+                                 k_ring=kr, v_ring=vr, n_sink=s, window=W)
+            else:
+                P.commit_kv(shape, dk, dv, dtab, dseq, kl[t], vl[t], kf[t], vf[t], flags, True, ws_c)
 
     def reset():
         dk.copy_(k0)
         dv.copy_(v0)
         dseq.copy_(seq_init)
+        if ring:
+            P.ring_fill(shape, dk, dv, dtab, dseq, s, W, kr, vr)
         ctr.zero_()
         outs.zero_()
         lses.zero_()
